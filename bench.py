@@ -1,0 +1,173 @@
+"""Throughput of the task-guided prefill-time eviction path on one MI355X.
+
+A step is one pass of the whole path (guide scores, V scales + quantisation, combine +
+top-k, compaction) over the workload, with inputs resident in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b_128k]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "context tokens compressed/sec (all layers+heads); achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(w, kept_total_per_head):
+    """Compulsory HBM bytes of each step, per kernel and in total (see the design notes)."""
+    from paper_2608_03276_amd import binding as B
+
+    LH = w.L * w.Hkv
+    n = w.n_tot
+    d = w.d
+    rb = B.row_bytes(w.qfmt, w.bits, d)
+    kt = kept_total_per_head
+    q_bytes = w.L * w.Hq * w.g_tot * d * 2
+    per = {
+        "tp_guide_scores": LH * n * (2 * d + 4) + q_bytes,          # read K once, write s_key
+        "tp_quantize_v_scales": LH * n * (2 * d + rb + 4),         # read V, write qV and scales
+        "tp_combine_select_topk": LH * (n * (4 + 4 + 4) + kt * 4),  # read s_key, scales; write S, kept idx
+        "tp_compact_kv": LH * kt * (2 * (2 * d + rb + 4) + 4),     # read kept rows + idx, write them
+    }
+    path = LH * (n * (2 * d + 2 * d + rb + 4) + kt * (2 * d + rb + 4 + 2 * d + rb + 4 + 4)) + q_bytes
+    return per, path
+
+
+def cpu_baseline(w, seconds: float):
+    """The CPU oracle (test infrastructure) timed on a bounded sample of segments."""
+    import numpy as np
+    import threadpoolctl
+
+    from oracle import taskpress_oracle as o
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity_util as pu
+
+    segs = [(b, l, h) for b in range(w.batch) for l in range(w.L) for h in range(w.Hkv)]
+    rng = np.random.default_rng(0)
+    order = rng.permutation(len(segs))
+    done_tokens = 0
+    done = 0
+    elapsed = 0.0
+    for i in order:
+        b, l, h = segs[i]
+        qg, kb, vb = pu.host_segment(w, b, l, h)  # input generation is not timed
+        k = o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget)
+        t0 = time.perf_counter()
+        o.evict_segment(qg, kb, vb, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                        rule=w.rule, k=k)
+        elapsed += time.perf_counter() - t0
+        done += 1
+        done_tokens += w.ctx_lens[b]
+        if elapsed >= seconds:
+            break
+    # a context token counts once all L * Hkv segments of it are done
+    tokens_equiv = done_tokens / (w.L * w.Hkv)
+    threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
+    return {"value": tokens_equiv / elapsed, "unit": "context tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {len(segs)} (sequence, layer, KV head) segments, {elapsed:.1f} s of oracle time "
+                      f"(numpy float64; BLAS threads = cores)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_128k")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the path shards by "
+              f"(layer, KV head, sequence) with no communication, see the design notes.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_03276_amd import binding as B
+    from synth import workloads as W
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity_util as pu
+
+    w = W.ALL[args.workload]()
+    torch.cuda.set_device(0)
+    q, k, v = pu.device_inputs(w)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    ko = B.kept_offsets_for(bt, w.keep_ratio or 0.0, w.keep_budget or 0)
+    bufs = B.EvictBuffers(d, bt, w.qfmt, w.bits, ko)
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        s = torch.cuda.current_stream()
+        if ev: ev[0].record(s)
+        B.tp_guide_scores(d, bt, q, k, w.softmax_scale, w.pool_k, bufs.s_key, bufs.ws_guide)
+        if ev: ev[1].record(s)
+        B.tp_quantize_v_scales(d, bt, v, w.qfmt, w.bits, bufs.scales, bufs.v_q)
+        if ev: ev[2].record(s)
+        B.tp_combine_select_topk(d, bt, bufs.s_key, bufs.scales, w.rule, w.keep_ratio or 0.0, w.keep_budget or 0,
+                                 ko, bufs.kept_idx, bufs.s_comb)
+        if ev: ev[3].record(s)
+        B.tp_compact_kv(d, bt, ko, bufs.kept_idx, k, bufs.v_q, bufs.scales, w.qfmt, w.bits, bufs.k_c, bufs.v_q_c,
+                        bufs.scales_c)
+        if ev: ev[4].record(s)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    names = ["tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv"]
+    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(names)}
+
+    per, path_bytes = algorithmic_bytes(w, ko[-1])
+    dom = max(stage_ms, key=stage_ms.get)
+    achieved = per[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "algorithmic_bytes": per[dom], "avg_ms": round(stage_ms[dom], 4)}
+    path_gbs = path_bytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(w.n_tot / (ms * 1e-3), 1),
+        "unit": "context tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
+        "config": {"workload": w.describe(), "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
+                   "context_tokens": w.n_tot, "guide_tokens": w.g_tot, "kept_per_head": ko[-1]},
+        "roofline": roofline,
+        "path_hbm": {"achieved": round(path_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(path_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": path_bytes},
+        "stages_ms": {n: round(t, 4) for n, t in stage_ms.items()},
+    }
+    del q, k, v, bufs
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,195 @@
+/*
+ * taskpress.h — C ABI of the task-guided prefill-time KV-cache eviction path
+ * (TaskPress, arXiv 2608.03276) for AMD Instinct MI355X (gfx950).
+ *
+ * The path, per (sequence, layer, KV head) "segment":
+ *   1. tp_guide_scores        key score s_key of Eq. 1 (Sec. 3.2): softmax attention
+ *                             of the task-guide queries on the context keys, summed
+ *                             over guide tokens, averaged over the GQA group, pooled.
+ *   2. tp_quantize_v_scales   value score gamma of Eq. 2 (Sec. 3.3): the per-token
+ *                             quantisation scale, fused with quantising V.
+ *   3. tp_combine_select_topk combined score of Eq. 3 (Sec. 3.4) and the top-k kept
+ *                             index set I per KV head (uniform budget, Sec. 4 setup).
+ *   4. tp_compact_kv          gather of the kept K rows, quantised V rows and scales
+ *                             (the evicted tokens and the guide's KV are dropped).
+ *
+ * Conventions (every entry point):
+ *  - Returns tp_status.  All arguments are validated on the host before any GPU
+ *    work is enqueued; on error nothing is enqueued and tp_last_error() describes
+ *    the problem (thread-local, valid until the next call on the same thread).
+ *  - Tensor pointers are DEVICE pointers; shape / offset arrays are HOST pointers.
+ *    `stream` is a hipStream_t (NULL = the default stream).
+ *  - Ownership: the caller allocates every input, output and workspace buffer.
+ *    The library allocates nothing and keeps no pointer after returning; buffers
+ *    must stay valid until the enqueued work has completed.
+ *  - Execution is asynchronous and stream-ordered; nothing synchronises inside a
+ *    call.  Calls are re-entrant.  Results are bit-identical from run to run (no
+ *    floating-point atomics; fixed reduction orders).
+ *  - Layouts are row-major and contiguous, head-major, so each segment is one
+ *    contiguous block; sequences of a batch sit back to back along the token axis:
+ *      q_guide   bf16 [L][Hq][G_tot][d]
+ *      k, v      bf16 [L][Hkv][N_tot][d]
+ *      per-token fp32 [L][Hkv][N_tot]            (s_key, scales, combined score)
+ *      v_q       bytes [L][Hkv][N_tot][row_bytes] (row_bytes = d, or d/2 for int b<=4)
+ *      kept      int32 [L][Hkv][K_tot]  and  [L][Hkv][K_tot][d] / [..][row_bytes]
+ *    Query head r belongs to KV head r / (Hq/Hkv) (grouped-query attention).
+ *  - Inputs are finite (no NaN/Inf).  bf16 values are raw bit patterns (uint16).
+ */
+#ifndef TASKPRESS_H
+#define TASKPRESS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tp_status;
+enum {
+  TP_OK = 0,
+  TP_ERR_NULL = 1,        /* a required pointer is NULL */
+  TP_ERR_SHAPE = 2,       /* inconsistent dims, offsets or sizes */
+  TP_ERR_PARAM = 3,       /* a scalar parameter is out of its domain */
+  TP_ERR_UNSUPPORTED = 4, /* valid but not implemented here (e.g. head_dim, batch size) */
+  TP_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than tp_workspace_size() */
+  TP_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+};
+
+/* Quantisation format of V (Eq. 2 and Sec. 4 setup). */
+enum {
+  TP_QFMT_INT = 0,     /* symmetric b-bit integers, qmax = 2^(b-1)-1, b in [2, 8];
+                          b <= 4 packs two values per byte (even element in the low nibble,
+                          4-bit two's complement), otherwise one int8 per value */
+  TP_QFMT_FP8_E4M3 = 1 /* OCP E4M3 codes, qmax = 448; `bits` is ignored */
+};
+
+/* Combination rule of the key and value scores. */
+enum {
+  TP_COMBINE_MUL = 0,      /* s = s_key * gamma (Eq. 3, the method's rule) */
+  TP_COMBINE_NORM_ADD = 1, /* s = s_key/||s_key||_2 + gamma/||gamma||_2 (aggregation table, Sec. 4.4) */
+  TP_COMBINE_HARMONIC = 2, /* s = 2 s_key gamma / (s_key + gamma), 0 if both are 0 (same table) */
+  TP_COMBINE_KEY_ONLY = 3  /* s = s_key (key-score-only ablation, Sec. 4.3) */
+};
+
+/* Entry points that take a workspace (argument of tp_workspace_size). */
+enum { TP_FN_GUIDE_SCORES = 0, TP_FN_COMBINE_SELECT_TOPK = 1 };
+
+typedef struct tp_dims {
+  int32_t num_layers;   /* L   >= 1 */
+  int32_t num_q_heads;  /* Hq  >= 1, a multiple of Hkv */
+  int32_t num_kv_heads; /* Hkv >= 1 */
+  int32_t head_dim;     /* d: 64 or 128 */
+} tp_dims;
+
+#define TP_MAX_BATCH 64
+
+typedef struct tp_batch {
+  int32_t batch;                /* B in [1, TP_MAX_BATCH] */
+  const int64_t* ctx_offsets;   /* host [B+1]: sequence b owns context tokens
+                                   [ctx_offsets[b], ctx_offsets[b+1]); ctx_offsets[0] = 0,
+                                   N_b = difference >= 1, N_tot = ctx_offsets[B] */
+  const int64_t* guide_offsets; /* host [B+1]: guide tokens of sequence b, G_b >= 1 (for
+                                   tp_guide_scores; may be NULL for the other calls) */
+} tp_batch;
+
+/* Version string of the library. */
+const char* tp_version(void);
+
+/* Human-readable name of a status code. */
+const char* tp_status_string(tp_status s);
+
+/* Detail message of the last error on this thread ("" after a successful call). */
+const char* tp_last_error(void);
+
+/*
+ * Size of the kept set of one KV head (problem statement, Sec. 3.1; uniform
+ * per-head budget, Sec. 4 setup).  Exactly one of keep_ratio / keep_budget is
+ * used: keep_ratio in (0, 1] (= 1 - eviction ratio) gives
+ * k = max(1, floor(n * keep_ratio)) computed in binary64; keep_ratio <= 0 selects
+ * the budget, k = min(keep_budget, n).  Returns -1 if n < 1 or neither / both
+ * are valid.  Host only.
+ */
+int64_t tp_keep_count(int64_t n, double keep_ratio, int64_t keep_budget);
+
+/*
+ * Bytes of device workspace `fn` needs for these dims / batch (host only).
+ * TP_FN_GUIDE_SCORES needs guide_offsets; TP_FN_COMBINE_SELECT_TOPK does not.
+ */
+tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* batch, size_t* bytes);
+
+/*
+ * Step 1 — key score of Eq. 1 (Sec. 3.2), for every (sequence b, layer l, KV head h):
+ *   A^(r)[j][i] = softmax_i( softmax_scale * <q_guide[l][r][g0+j], k[l][h][n0+i]> )
+ *                 over the N_b context tokens i of sequence b (softmax-normalised as
+ *                 stated in Sec. 6; the guide's own keys are not part of the normaliser),
+ *   raw[i]      = (1/R) * sum over the R query heads r of KV head h, sum_{j<G_b} A^(r)[j][i],
+ *   s_key[l][h][n0+i] = (1/pool_k) * sum_{|t| <= pool_k/2} raw[i+t], raw = 0 outside [0, N_b).
+ * q_guide bf16 [L][Hq][G_tot][d], k bf16 [L][Hkv][N_tot][d], s_key fp32 [L][Hkv][N_tot] (out).
+ * softmax_scale > 0 (callers pass 1/sqrt(d)); pool_k odd, >= 1.
+ * workspace: device, >= tp_workspace_size(TP_FN_GUIDE_SCORES, ...) bytes, 256-byte aligned.
+ * Errors: TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE,
+ * TP_ERR_HIP.
+ */
+tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void* q_guide,
+                          const void* k, float softmax_scale, int32_t pool_k, float* s_key,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Step 2 — value score of Eq. 2 (Sec. 3.3), fused with per-token quantisation of V
+ * (KIVI-style per-token scheme cited in Sec. 3.3; int4 cache of Sec. 4 setup):
+ *   gamma[l][h][t] = fl32( max_c |v[l][h][t][c]| / qmax )
+ *   q[l][h][t][c]  = clamp(RNE(fl32(v / gamma)), -qmax, qmax)   (TP_QFMT_INT), or the OCP E4M3
+ *                    code of fl32(v / gamma), round-to-nearest-even, saturating at 448
+ *                    (TP_QFMT_FP8_E4M3); rows with gamma = 0 give q = 0.
+ * Independent of the batch split (every token of N_tot is processed); `batch` only
+ * provides N_tot.  v bf16 [L][Hkv][N_tot][d]; scales fp32 [L][Hkv][N_tot] (out);
+ * v_q bytes [L][Hkv][N_tot][row_bytes] (out) or NULL to compute the scales only.
+ * Errors: TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM (qfmt, bits), TP_ERR_UNSUPPORTED, TP_ERR_HIP.
+ */
+tp_status tp_quantize_v_scales(const tp_dims* dims, const tp_batch* batch, const void* v,
+                               int32_t qfmt, int32_t bits, float* scales, void* v_q,
+                               void* stream);
+
+/*
+ * Step 3 — combined score (Eq. 3, or a variant from the aggregation table) and the
+ * kept index set I of every (sequence, layer, KV head) (Sec. 3.4; uniform budget,
+ * selected per head independently, Sec. 4 setup):
+ *   S[i] = combine(s_key[i], scales[i]) stored as fp32 (TP_COMBINE_*),
+ *   k_b  = tp_keep_count(N_b, keep_ratio, keep_budget),
+ *   I    = the k_b indices with the largest S, ties broken towards the lower index,
+ *          written in ascending order as sequence-local token indices in [0, N_b).
+ * s_key, scales fp32 [L][Hkv][N_tot], all finite and >= 0.
+ * kept_offsets: host [B+1], must equal the prefix sums of k_b (TP_ERR_SHAPE otherwise);
+ * kept_idx int32 [L][Hkv][K_tot] (out), K_tot = kept_offsets[B];
+ * s_out fp32 [L][Hkv][N_tot] (out, optional): the combined scores S.
+ * workspace: >= tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, ...) bytes.
+ * Exactly one of keep_ratio in (0, 1] / keep_budget >= 1 must be given (the other
+ * <= 0), otherwise TP_ERR_PARAM.
+ */
+tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, const float* s_key,
+                                 const float* scales, int32_t rule, double keep_ratio,
+                                 int64_t keep_budget, const int64_t* kept_offsets,
+                                 int32_t* kept_idx, float* s_out, void* workspace,
+                                 size_t ws_bytes, void* stream);
+
+/*
+ * Step 4 — compaction (Sec. 3.1: only I is kept; Sec. 4 setup: eviction after
+ * prefill, the guide's KV discarded — it is not part of k / v here):
+ *   k_out[l][h][ko_b + t][:]      = k[l][h][n0_b + kept_idx[l][h][ko_b + t]][:]
+ *   v_q_out[l][h][ko_b + t][:]    = v_q[l][h][n0_b + idx][:]       (row_bytes bytes)
+ *   scales_out[l][h][ko_b + t]    = scales[l][h][n0_b + idx]
+ * for t < kept_offsets[b+1] - kept_offsets[b] (= ko_{b+1} - ko_b <= N_b).  qfmt/bits give
+ * row_bytes.  An index outside [0, N_b) yields a zero row and zero scale (no fault).
+ * v_q/v_q_out and scales/scales_out may be NULL pairwise to skip that output.
+ */
+tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                        const int32_t* kept_idx, const void* k, const void* v_q,
+                        const float* scales, int32_t qfmt, int32_t bits, void* k_out,
+                        void* v_q_out, float* scales_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TASKPRESS_H */

@@ -1,0 +1,262 @@
+"""ctypes binding of libtaskpress (include/taskpress.h): argument marshalling only.
+
+Every step of the eviction path runs in the library's HIP kernels; PyTorch only
+provides device memory and the current HIP stream.  Importing this module on a
+machine without the built library raises ImportError (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libtaskpress.so")
+
+TP_OK, TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE, TP_ERR_HIP = range(7)
+TP_QFMT_INT, TP_QFMT_FP8_E4M3 = 0, 1
+TP_COMBINE_MUL, TP_COMBINE_NORM_ADD, TP_COMBINE_HARMONIC, TP_COMBINE_KEY_ONLY = 0, 1, 2, 3
+TP_FN_GUIDE_SCORES, TP_FN_COMBINE_SELECT_TOPK = 0, 1
+TP_MAX_BATCH = 64
+
+EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
+            "tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv")
+
+
+class TaskPressError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_STATUS_NAMES = {0: "TP_OK", 1: "TP_ERR_NULL", 2: "TP_ERR_SHAPE", 3: "TP_ERR_PARAM", 4: "TP_ERR_UNSUPPORTED",
+                 5: "TP_ERR_WORKSPACE", 6: "TP_ERR_HIP"}
+
+
+class TpDims(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+
+
+class TpBatch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("ctx_offsets", ctypes.POINTER(ctypes.c_int64)),
+                ("guide_offsets", ctypes.POINTER(ctypes.c_int64))]
+
+
+def _i64_array(vals):
+    vals = [int(v) for v in vals]
+    return (ctypes.c_int64 * len(vals))(*vals)
+
+
+class Batch:
+    """A tp_batch plus the host offset arrays it points to (kept alive here)."""
+
+    def __init__(self, ctx_offsets, guide_offsets=None):
+        self.ctx_offsets = [int(x) for x in ctx_offsets]
+        self.guide_offsets = None if guide_offsets is None else [int(x) for x in guide_offsets]
+        self._ctx = _i64_array(self.ctx_offsets)
+        self._g = None if guide_offsets is None else _i64_array(self.guide_offsets)
+        self.c = TpBatch(len(self.ctx_offsets) - 1, self._ctx,
+                         self._g if self._g is not None else ctypes.POINTER(ctypes.c_int64)())
+
+    @property
+    def batch(self):
+        return len(self.ctx_offsets) - 1
+
+    @property
+    def n_tot(self):
+        return self.ctx_offsets[-1]
+
+    @property
+    def g_tot(self):
+        return self.guide_offsets[-1]
+
+
+def dims(L, Hq, Hkv, d) -> TpDims:
+    return TpDims(L, Hq, Hkv, d)
+
+
+_lib = None
+
+
+def load():
+    """Load libtaskpress.so (raises ImportError when it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    pd, pb = ctypes.POINTER(TpDims), ctypes.POINTER(TpBatch)
+    pi64 = ctypes.POINTER(ctypes.c_int64)
+    lib.tp_version.restype = ctypes.c_char_p
+    lib.tp_version.argtypes = []
+    lib.tp_status_string.restype = ctypes.c_char_p
+    lib.tp_status_string.argtypes = [ctypes.c_int32]
+    lib.tp_last_error.restype = ctypes.c_char_p
+    lib.tp_last_error.argtypes = []
+    lib.tp_keep_count.restype = ctypes.c_int64
+    lib.tp_keep_count.argtypes = [ctypes.c_int64, ctypes.c_double, ctypes.c_int64]
+    lib.tp_workspace_size.restype = ctypes.c_int32
+    lib.tp_workspace_size.argtypes = [ctypes.c_int32, pd, pb, ctypes.POINTER(ctypes.c_size_t)]
+    lib.tp_guide_scores.restype = ctypes.c_int32
+    lib.tp_guide_scores.argtypes = [pd, pb, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
+    lib.tp_quantize_v_scales.restype = ctypes.c_int32
+    lib.tp_quantize_v_scales.argtypes = [pd, pb, P, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    lib.tp_combine_select_topk.restype = ctypes.c_int32
+    lib.tp_combine_select_topk.argtypes = [pd, pb, P, P, ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64,
+                                           P, P, P, ctypes.c_size_t, P]
+    lib.tp_compact_kv.restype = ctypes.c_int32
+    lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != TP_OK:
+        raise TaskPressError(status, load().tp_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _need(t, numel, name, device=True):
+    if t is None:
+        return
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if device and not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.numel() * t.element_size() < numel:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, needs {numel}")
+
+
+# ----------------------------------------------------------------------------- entry points
+def tp_version() -> str:
+    return load().tp_version().decode()
+
+
+def tp_keep_count(n: int, keep_ratio: float = 0.0, keep_budget: int = 0) -> int:
+    return int(load().tp_keep_count(int(n), float(keep_ratio), int(keep_budget)))
+
+
+def tp_workspace_size(fn: int, d: TpDims, batch: Batch) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().tp_workspace_size(fn, ctypes.byref(d), ctypes.byref(batch.c), ctypes.byref(out)))
+    return int(out.value)
+
+
+def tp_guide_scores(d: TpDims, batch: Batch, q_guide, k, softmax_scale: float, pool_k: int, s_key, workspace,
+                    stream=None):
+    L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
+    _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(s_key, L * Hkv * batch.n_tot * 4, "s_key")
+    _check(load().tp_guide_scores(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k),
+                                  float(softmax_scale), int(pool_k), _ptr(s_key), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size() if workspace is not None else 0,
+                                  _stream(stream)))
+
+
+def row_bytes(qfmt: int, bits: int, head_dim: int) -> int:
+    return head_dim // 2 if (qfmt == TP_QFMT_INT and bits <= 4) else head_dim
+
+
+def tp_quantize_v_scales(d: TpDims, batch: Batch, v, qfmt: int, bits: int, scales, v_q=None, stream=None):
+    L, Hkv, D = d.num_layers, d.num_kv_heads, d.head_dim
+    _need(v, L * Hkv * batch.n_tot * D * 2, "v")
+    _need(scales, L * Hkv * batch.n_tot * 4, "scales")
+    _need(v_q, L * Hkv * batch.n_tot * row_bytes(qfmt, bits, D), "v_q")
+    _check(load().tp_quantize_v_scales(ctypes.byref(d), ctypes.byref(batch.c), _ptr(v), int(qfmt), int(bits),
+                                       _ptr(scales), _ptr(v_q), _stream(stream)))
+
+
+def kept_offsets_for(batch: Batch, keep_ratio: float = 0.0, keep_budget: int = 0):
+    out = [0]
+    for b in range(batch.batch):
+        n = batch.ctx_offsets[b + 1] - batch.ctx_offsets[b]
+        out.append(out[-1] + tp_keep_count(n, keep_ratio, keep_budget))
+    return out
+
+
+def tp_combine_select_topk(d: TpDims, batch: Batch, s_key, scales, rule: int, keep_ratio: float, keep_budget: int,
+                           kept_offsets, kept_idx, s_out=None, workspace=None, stream=None):
+    L, Hkv = d.num_layers, d.num_kv_heads
+    _need(s_key, L * Hkv * batch.n_tot * 4, "s_key")
+    _need(scales, L * Hkv * batch.n_tot * 4, "scales")
+    _need(kept_idx, L * Hkv * int(kept_offsets[-1]) * 4, "kept_idx")
+    _need(s_out, L * Hkv * batch.n_tot * 4, "s_out")
+    ko = _i64_array(kept_offsets)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().tp_combine_select_topk(ctypes.byref(d), ctypes.byref(batch.c), _ptr(s_key), _ptr(scales),
+                                         int(rule), float(keep_ratio), int(keep_budget), ko, _ptr(kept_idx),
+                                         _ptr(s_out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def tp_compact_kv(d: TpDims, batch: Batch, kept_offsets, kept_idx, k, v_q, scales, qfmt: int, bits: int, k_out,
+                  v_q_out, scales_out, stream=None):
+    L, Hkv, D = d.num_layers, d.num_kv_heads, d.head_dim
+    kt = int(kept_offsets[-1])
+    _need(kept_idx, L * Hkv * kt * 4, "kept_idx")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(k_out, L * Hkv * kt * D * 2, "k_out")
+    _need(v_q, L * Hkv * batch.n_tot * row_bytes(qfmt, bits, D), "v_q")
+    _need(v_q_out, L * Hkv * kt * row_bytes(qfmt, bits, D), "v_q_out")
+    _need(scales, L * Hkv * batch.n_tot * 4, "scales")
+    _need(scales_out, L * Hkv * kt * 4, "scales_out")
+    ko = _i64_array(kept_offsets)
+    _check(load().tp_compact_kv(ctypes.byref(d), ctypes.byref(batch.c), ko, _ptr(kept_idx), _ptr(k), _ptr(v_q),
+                                _ptr(scales), int(qfmt), int(bits), _ptr(k_out), _ptr(v_q_out), _ptr(scales_out),
+                                _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- whole path
+class EvictBuffers:
+    """Device buffers of one eviction: outputs and workspaces, allocated once and reused."""
+
+    def __init__(self, d: TpDims, batch: Batch, qfmt: int, bits: int, kept_offsets, device="cuda"):
+        L, Hkv, D = d.num_layers, d.num_kv_heads, d.head_dim
+        n, kt = batch.n_tot, int(kept_offsets[-1])
+        rb = row_bytes(qfmt, bits, D)
+        self.kept_offsets = list(kept_offsets)
+        self.s_key = torch.empty(L * Hkv * n, dtype=torch.float32, device=device)
+        self.scales = torch.empty(L * Hkv * n, dtype=torch.float32, device=device)
+        self.v_q = torch.empty(L * Hkv * n * rb, dtype=torch.uint8, device=device)
+        self.s_comb = torch.empty(L * Hkv * n, dtype=torch.float32, device=device)
+        self.kept_idx = torch.empty(L * Hkv * max(kt, 1), dtype=torch.int32, device=device)
+        self.k_c = torch.empty(L * Hkv * max(kt, 1) * D, dtype=torch.bfloat16, device=device)
+        self.v_q_c = torch.empty(L * Hkv * max(kt, 1) * rb, dtype=torch.uint8, device=device)
+        self.scales_c = torch.empty(L * Hkv * max(kt, 1), dtype=torch.float32, device=device)
+        self.ws_guide = torch.empty(tp_workspace_size(TP_FN_GUIDE_SCORES, d, batch), dtype=torch.uint8,
+                                    device=device)
+
+
+def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
+          rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0, bufs: EvictBuffers = None,
+          stream=None) -> EvictBuffers:
+    """Run the four steps on one stream; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
+    ko = kept_offsets_for(batch, keep_ratio, keep_budget)
+    if bufs is None:
+        bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
+    tp_guide_scores(d, batch, q_guide, k, softmax_scale, pool_k, bufs.s_key, bufs.ws_guide, stream)
+    tp_quantize_v_scales(d, batch, v, qfmt, bits, bufs.scales, bufs.v_q, stream)
+    tp_combine_select_topk(d, batch, bufs.s_key, bufs.scales, rule, keep_ratio, keep_budget, ko, bufs.kept_idx,
+                           bufs.s_comb, None, stream)
+    tp_compact_kv(d, batch, ko, bufs.kept_idx, k, bufs.v_q, bufs.scales, qfmt, bits, bufs.k_c, bufs.v_q_c,
+                  bufs.scales_c, stream)
+    return bufs

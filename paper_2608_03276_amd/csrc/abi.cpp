@@ -1,0 +1,335 @@
+// C-ABI layer of libtaskpress: synchronous host-side validation, workspace layout and
+// kernel dispatch.  Nothing is enqueued unless every argument is valid.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+
+#include "tp_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+tp_status fail(tp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+tp_status ok() {
+  g_err.clear();
+  return TP_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+tp_status check_dims(const tp_dims* d) {
+  if (!d) return fail(TP_ERR_NULL, "dims is NULL");
+  if (d->num_layers < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 || d->head_dim < 1)
+    return fail(TP_ERR_SHAPE, "dims must be positive (L=%d Hq=%d Hkv=%d d=%d)", d->num_layers,
+                d->num_q_heads, d->num_kv_heads, d->head_dim);
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(TP_ERR_SHAPE, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(TP_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d->head_dim);
+  if ((int64_t)d->num_layers * d->num_kv_heads > 65535)
+    return fail(TP_ERR_UNSUPPORTED, "num_layers * num_kv_heads exceeds 65535");
+  return TP_OK;
+}
+
+tp_status check_offsets(const int64_t* off, int32_t batch, const char* what, bool allow_empty_seq) {
+  if (!off) return fail(TP_ERR_NULL, "%s is NULL", what);
+  if (off[0] != 0) return fail(TP_ERR_SHAPE, "%s[0] must be 0", what);
+  for (int b = 0; b < batch; ++b) {
+    const int64_t n = off[b + 1] - off[b];
+    if (n < (allow_empty_seq ? 0 : 1))
+      return fail(TP_ERR_SHAPE, "%s: entry %d has length %lld", what, b, (long long)n);
+  }
+  return TP_OK;
+}
+
+tp_status check_batch(const tp_batch* bt, bool need_guides) {
+  if (!bt) return fail(TP_ERR_NULL, "batch is NULL");
+  if (bt->batch < 1) return fail(TP_ERR_SHAPE, "batch must be >= 1");
+  if (bt->batch > TP_MAX_BATCH)
+    return fail(TP_ERR_UNSUPPORTED, "batch %d exceeds TP_MAX_BATCH (%d)", bt->batch, TP_MAX_BATCH);
+  tp_status s = check_offsets(bt->ctx_offsets, bt->batch, "ctx_offsets", false);
+  if (s != TP_OK) return s;
+  if (need_guides) {
+    s = check_offsets(bt->guide_offsets, bt->batch, "guide_offsets", false);
+    if (s != TP_OK) return s;
+  }
+  return TP_OK;
+}
+
+tp::BatchArgs batch_args(const tp_batch* bt, bool with_guides) {
+  tp::BatchArgs a;
+  memset(&a, 0, sizeof a);
+  a.batch = bt->batch;
+  for (int b = 0; b <= bt->batch; ++b) {
+    a.ctx_off[b] = bt->ctx_offsets[b];
+    a.g_off[b] = with_guides ? bt->guide_offsets[b] : 0;
+  }
+  return a;
+}
+
+tp_status hip_fail(hipError_t e, const char* where) {
+  return fail(TP_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+size_t select_workspace(const tp_dims* d, const tp_batch* bt) {
+  const size_t n = (size_t)d->num_layers * d->num_kv_heads * (size_t)bt->ctx_offsets[bt->batch];
+  return ((n * sizeof(float)) + 255) & ~(size_t)255;
+}
+
+int row_bytes_of(int32_t qfmt, int32_t bits, int32_t d) {
+  return (qfmt == TP_QFMT_INT && bits <= 4) ? d / 2 : d;
+}
+
+tp_status check_qfmt(int32_t qfmt, int32_t bits) {
+  if (qfmt == TP_QFMT_INT) {
+    if (bits < 2 || bits > 8) return fail(TP_ERR_PARAM, "bits %d outside [2, 8]", bits);
+    return TP_OK;
+  }
+  if (qfmt == TP_QFMT_FP8_E4M3) return TP_OK;
+  return fail(TP_ERR_PARAM, "unknown qfmt %d", qfmt);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tp_version(void) { return "taskpress-mi355x 0.1.0 (gfx950)"; }
+
+const char* tp_status_string(tp_status s) {
+  switch (s) {
+    case TP_OK: return "TP_OK";
+    case TP_ERR_NULL: return "TP_ERR_NULL";
+    case TP_ERR_SHAPE: return "TP_ERR_SHAPE";
+    case TP_ERR_PARAM: return "TP_ERR_PARAM";
+    case TP_ERR_UNSUPPORTED: return "TP_ERR_UNSUPPORTED";
+    case TP_ERR_WORKSPACE: return "TP_ERR_WORKSPACE";
+    case TP_ERR_HIP: return "TP_ERR_HIP";
+    default: return "TP_ERR_UNKNOWN";
+  }
+}
+
+const char* tp_last_error(void) { return g_err.c_str(); }
+
+int64_t tp_keep_count(int64_t n, double keep_ratio, int64_t keep_budget) {
+  if (n < 1) return -1;
+  const bool use_ratio = keep_ratio > 0.0;
+  const bool use_budget = keep_budget >= 1;
+  if (use_ratio == use_budget) return -1;
+  if (use_ratio) {
+    if (!(keep_ratio <= 1.0)) return -1;
+    const int64_t k = (int64_t)floor((double)n * keep_ratio);
+    return k < 1 ? 1 : k;
+  }
+  return keep_budget < n ? keep_budget : n;
+}
+
+tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* batch, size_t* bytes) {
+  if (!bytes) return fail(TP_ERR_NULL, "bytes is NULL");
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  if (fn == TP_FN_GUIDE_SCORES) {
+    s = check_batch(batch, true);
+    if (s != TP_OK) return s;
+    *bytes = tp::guide_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads,
+                                        batch->ctx_offsets, batch->guide_offsets, batch->batch)
+                 .total;
+    return ok();
+  }
+  if (fn == TP_FN_COMBINE_SELECT_TOPK) {
+    s = check_batch(batch, false);
+    if (s != TP_OK) return s;
+    *bytes = select_workspace(dims, batch);
+    return ok();
+  }
+  return fail(TP_ERR_PARAM, "unknown function id %d", fn);
+}
+
+tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                          float softmax_scale, int32_t pool_k, float* s_key, void* workspace,
+                          size_t ws_bytes, void* stream) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, true);
+  if (s != TP_OK) return s;
+  if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
+  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
+    return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
+  if (pool_k < 1 || (pool_k & 1) == 0) return fail(TP_ERR_PARAM, "pool_k must be odd and >= 1 (got %d)", pool_k);
+  const tp::GuideWorkspace lay = tp::guide_workspace_layout(
+      dims->num_layers, dims->num_q_heads, dims->num_kv_heads, batch->ctx_offsets, batch->guide_offsets, batch->batch);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu%s)", lay.total, ws_bytes,
+                workspace ? "" : ", NULL");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(TP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  tp::GuideArgs a;
+  memset(&a, 0, sizeof a);
+  a.bt = batch_args(batch, true);
+  int64_t max_nb = 0, max_gb = 0;
+  for (int b = 0; b < batch->batch; ++b) {
+    max_nb = std::max<int64_t>(max_nb, batch->ctx_offsets[b + 1] - batch->ctx_offsets[b]);
+    max_gb = std::max<int64_t>(max_gb, batch->guide_offsets[b + 1] - batch->guide_offsets[b]);
+  }
+  a.q = (const uint16_t*)q_guide;
+  a.k = (const uint16_t*)k;
+  a.s_key = s_key;
+  a.stats = (float2*)((char*)workspace + lay.stats_off);
+  a.lse2 = (float*)((char*)workspace + lay.lse_off);
+  a.raw = (float*)((char*)workspace + lay.raw_off);
+  a.L = dims->num_layers;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.R = dims->num_q_heads / dims->num_kv_heads;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.g_tot = batch->guide_offsets[batch->batch];
+  a.c = (float)((double)softmax_scale * 1.4426950408889634);
+  a.pool_inv = (float)(1.0 / ((double)a.R * pool_k));
+  a.pool_half = pool_k / 2;
+  a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
+  a.nchunk_pad = (a.nchunk_max + 7) & ~7;
+  a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
+  if ((int64_t)a.nchunk_pad * a.nrg_max > 0x7FFFFFFF)
+    return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
+  const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_guide_scores launch");
+  return ok();
+}
+
+tp_status tp_quantize_v_scales(const tp_dims* dims, const tp_batch* batch, const void* v, int32_t qfmt,
+                               int32_t bits, float* scales, void* v_q, void* stream) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  s = check_qfmt(qfmt, bits);
+  if (s != TP_OK) return s;
+  if (!v || !scales) return fail(TP_ERR_NULL, "v and scales must be non-NULL");
+  if (!aligned16(v) || !aligned16(scales) || (v_q && !aligned16(v_q)))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  tp::QuantArgs a;
+  a.v = (const uint16_t*)v;
+  a.scales = scales;
+  a.vq = (uint8_t*)v_q;
+  a.rows = (int64_t)dims->num_layers * dims->num_kv_heads * batch->ctx_offsets[batch->batch];
+  a.qfmt = qfmt;
+  a.bits = bits;
+  a.qmax = qfmt == TP_QFMT_INT ? (float)((1 << (bits - 1)) - 1) : 448.0f;
+  const hipError_t e = tp::launch_quantize(a, dims->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_quantize_v_scales launch");
+  return ok();
+}
+
+tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, const float* s_key,
+                                 const float* scales, int32_t rule, double keep_ratio, int64_t keep_budget,
+                                 const int64_t* kept_offsets, int32_t* kept_idx, float* s_out, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  if (!s_key || !scales || !kept_idx) return fail(TP_ERR_NULL, "s_key, scales and kept_idx must be non-NULL");
+  if (!aligned16(s_key) || !aligned16(scales) || !aligned16(kept_idx) || (s_out && !aligned16(s_out)))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (rule < TP_COMBINE_MUL || rule > TP_COMBINE_KEY_ONLY) return fail(TP_ERR_PARAM, "unknown rule %d", rule);
+  const bool use_ratio = keep_ratio > 0.0, use_budget = keep_budget >= 1;
+  if (use_ratio == use_budget)
+    return fail(TP_ERR_PARAM, "exactly one of keep_ratio in (0,1] and keep_budget >= 1 must be given");
+  if (use_ratio && !(keep_ratio <= 1.0)) return fail(TP_ERR_PARAM, "keep_ratio must be in (0, 1]");
+  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
+  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
+  tp::SelectArgs a;
+  memset(&a, 0, sizeof a);
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t kb = tp_keep_count(nb, keep_ratio, keep_budget);
+    if (kept_offsets[b + 1] - kept_offsets[b] != kb)
+      return fail(TP_ERR_SHAPE, "kept_offsets[%d+1]-kept_offsets[%d] = %lld, expected keep count %lld", b, b,
+                  (long long)(kept_offsets[b + 1] - kept_offsets[b]), (long long)kb);
+    a.k[b] = kb;
+    a.kept_off[b] = kept_offsets[b];
+  }
+  a.kept_off[batch->batch] = kept_offsets[batch->batch];
+  float* sbuf = s_out;
+  if (!sbuf) {
+    const size_t need = select_workspace(dims, batch);
+    if (!workspace || ws_bytes < need)
+      return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu)", need, ws_bytes);
+    if (!aligned16(workspace)) return fail(TP_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+    sbuf = (float*)workspace;
+  }
+  a.s_key = s_key;
+  a.scales = scales;
+  a.s_buf = sbuf;
+  a.kept = kept_idx;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.k_tot = kept_offsets[batch->batch];
+  a.rule = rule;
+  a.bt = batch_args(batch, false);
+  const hipError_t e =
+      tp::launch_select(a, dims->num_layers * dims->num_kv_heads, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk launch");
+  return ok();
+}
+
+tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                        const int32_t* kept_idx, const void* k, const void* v_q, const float* scales, int32_t qfmt,
+                        int32_t bits, void* k_out, void* v_q_out, float* scales_out, void* stream) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  s = check_qfmt(qfmt, bits);
+  if (s != TP_OK) return s;
+  if (!kept_idx || !k || !k_out) return fail(TP_ERR_NULL, "kept_idx, k and k_out must be non-NULL");
+  if ((v_q == nullptr) != (v_q_out == nullptr)) return fail(TP_ERR_NULL, "v_q and v_q_out must both be given or both NULL");
+  if ((scales == nullptr) != (scales_out == nullptr))
+    return fail(TP_ERR_NULL, "scales and scales_out must both be given or both NULL");
+  if (!aligned16(kept_idx) || !aligned16(k) || !aligned16(k_out) || (v_q && (!aligned16(v_q) || !aligned16(v_q_out))) ||
+      (scales && (!aligned16(scales) || !aligned16(scales_out))))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
+  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
+  tp::CompactArgs a;
+  memset(&a, 0, sizeof a);
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t kb = kept_offsets[b + 1] - kept_offsets[b];
+    if (kb < 0 || kb > nb)
+      return fail(TP_ERR_SHAPE, "kept count of sequence %d (%lld) outside [0, %lld]", b, (long long)kb, (long long)nb);
+    a.kept_off[b] = kept_offsets[b];
+  }
+  a.kept_off[batch->batch] = kept_offsets[batch->batch];
+  a.kept = kept_idx;
+  a.k = (const uint16_t*)k;
+  a.vq = (const uint8_t*)v_q;
+  a.scales = scales;
+  a.k_out = (uint16_t*)k_out;
+  a.vq_out = (uint8_t*)v_q_out;
+  a.scales_out = scales_out;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.k_tot = kept_offsets[batch->batch];
+  a.row_bytes = row_bytes_of(qfmt, bits, dims->head_dim);
+  a.bt = batch_args(batch, false);
+  const hipError_t e = tp::launch_compact(a, dims->num_layers * dims->num_kv_heads, dims->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_compact_kv launch");
+  return ok();
+}
+
+}  // extern "C"

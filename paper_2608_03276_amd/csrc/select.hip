@@ -1,0 +1,216 @@
+// Step 3 of the eviction path: the combined score (Eq. 3, or a variant from the
+// aggregation table of Sec. 4.4) and the top-k kept set of every (sequence, layer, KV head)
+// (Sec. 3.4; uniform per-head budget, Sec. 4 setup).
+//
+// One 1024-thread workgroup per segment.  The combined score S is written once (fp32) and
+// ranked through the order-preserving map of its bit pattern to uint32:
+//   - a 4-pass, 8-bit radix select finds the k-th largest key T and how many keys equal to
+//     T are needed (ties go to the lower index);
+//   - an ordered compaction then emits, in ascending token order, every index with key > T
+//     plus the first `need` indices with key == T: its output slot is
+//     #(key > T before i) + min(#(key == T before i), need), from one block-wide scan of a
+//     packed (greater, equal) count per tile.
+// Only integer LDS atomics (histogram counts) are used, so the result is deterministic.
+#include "tp_internal.h"
+
+namespace tp {
+namespace {
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kPerThread = 4;
+
+__device__ inline uint32_t order_key(float s) {
+  uint32_t b = __float_as_uint(s);
+  if (b == 0x80000000u) b = 0u;  // -0 ranks with +0
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ inline float combine(int rule, float s, float g, double na, double nb) {
+  switch (rule) {
+    case TP_COMBINE_KEY_ONLY:
+      return s;
+    case TP_COMBINE_HARMONIC: {
+      const double den = (double)s + (double)g;
+      return den > 0.0 ? (float)((2.0 * (double)s * (double)g) / den) : 0.0f;
+    }
+    case TP_COMBINE_NORM_ADD: {
+      const double ta = na > 0.0 ? (double)s / na : 0.0;
+      const double tb = nb > 0.0 ? (double)g / nb : 0.0;
+      return (float)(ta + tb);
+    }
+    default:
+      return s * g;
+  }
+}
+
+// Exclusive block scan of v (1024 threads); returns the prefix and sets `total`.
+__device__ inline uint32_t block_scan(uint32_t v, uint32_t* sh, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) sh[wave] = x;
+  __syncthreads();
+  if (wave == 0) {
+    const uint32_t w = lane < kSelWaves ? sh[lane] : 0u;
+    uint32_t s = w;
+#pragma unroll
+    for (int off = 1; off < kSelWaves; off <<= 1) {
+      const uint32_t y = __shfl_up(s, off);
+      if (lane >= off) s += y;
+    }
+    if (lane < kSelWaves) sh[lane] = s - w;
+    if (lane == kSelWaves - 1) sh[kSelWaves] = s;
+  }
+  __syncthreads();
+  const uint32_t r = x - v + sh[wave];
+  total = sh[kSelWaves];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
+  const int seg = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t n0 = a.bt.ctx_off[b];
+  const int64_t nb = a.bt.ctx_off[b + 1] - n0;
+  const int64_t k = a.k[b];
+  const float* sk = a.s_key + (int64_t)seg * a.n_tot + n0;
+  const float* sc = a.scales + (int64_t)seg * a.n_tot + n0;
+  float* sb = a.s_buf + (int64_t)seg * a.n_tot + n0;
+  int32_t* out = a.kept + (int64_t)seg * a.k_tot + a.kept_off[b];
+
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t scan_sh[kSelWaves + 1];
+  __shared__ double dred[kSelWaves][2];
+  __shared__ uint32_t sel_digit, sel_krem;
+
+  double norm_a = 0.0, norm_b = 0.0;
+  if (a.rule == TP_COMBINE_NORM_ADD) {
+    double s1 = 0.0, s2 = 0.0;
+    for (int64_t i = tid; i < nb; i += kSelThreads) {
+      const double x = sk[i], y = sc[i];
+      s1 += x * x;
+      s2 += y * y;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      s1 += __shfl_xor(s1, off);
+      s2 += __shfl_xor(s2, off);
+    }
+    if (lane == 0) {
+      dred[wave][0] = s1;
+      dred[wave][1] = s2;
+    }
+    __syncthreads();
+    double t1 = 0.0, t2 = 0.0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      t1 += dred[w][0];
+      t2 += dred[w][1];
+    }
+    norm_a = sqrt(t1);
+    norm_b = sqrt(t2);
+  }
+
+  for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
+  __syncthreads();
+  for (int64_t i = tid; i < nb; i += kSelThreads) {
+    const float S = combine(a.rule, sk[i], sc[i], norm_a, norm_b);
+    sb[i] = S;
+    atomicAdd(&hist[order_key(S) >> 24], 1u);
+  }
+  __syncthreads();
+
+  uint32_t prefix = 0, krem = (uint32_t)k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (pass > 0) {
+      for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
+      __syncthreads();
+      for (int64_t i = tid; i < nb; i += kSelThreads) {
+        const uint32_t key = order_key(sb[i]);
+        if ((key >> (shift + 8)) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+    }
+    if (wave == 0) {
+      // lane l owns digits 255-4l .. 252-4l, highest first
+      uint32_t c[4], lsum = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c[e] = hist[255 - 4 * lane - e];
+        lsum += c[e];
+      }
+      uint32_t incl = lsum;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+      }
+      const uint32_t excl = incl - lsum;
+      if (excl < krem && krem <= incl) {
+        uint32_t cum = excl;
+        for (int e = 0; e < 4; ++e) {
+          if (cum + c[e] >= krem) {
+            sel_digit = 255u - 4u * lane - e;
+            sel_krem = krem - cum;
+            break;
+          }
+          cum += c[e];
+        }
+      }
+    }
+    __syncthreads();
+    prefix = (prefix << 8) | sel_digit;
+    krem = sel_krem;
+    __syncthreads();
+  }
+  const uint32_t T = prefix, need = krem;
+
+  uint32_t gt_run = 0, eq_run = 0;
+  for (int64_t t0 = 0; t0 < nb; t0 += (int64_t)kSelThreads * kPerThread) {
+    const int64_t i0 = t0 + (int64_t)tid * kPerThread;
+    uint32_t keys[kPerThread];
+    uint32_t gtc = 0, eqc = 0;
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) {
+      const int64_t i = i0 + e;
+      keys[e] = i < nb ? order_key(sb[i]) : 0u;
+      if (i < nb) {
+        gtc += keys[e] > T;
+        eqc += keys[e] == T;
+      }
+    }
+    uint32_t total;
+    const uint32_t ex = block_scan((gtc << 16) | eqc, scan_sh, total);
+    uint32_t gx = gt_run + (ex >> 16), qx = eq_run + (ex & 0xFFFFu);
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) {
+      const int64_t i = i0 + e;
+      if (i >= nb) break;
+      if (keys[e] > T) {
+        const uint32_t pos = gx + (qx < need ? qx : need);
+        if (pos < (uint32_t)k) out[pos] = (int32_t)i;
+        ++gx;
+      } else if (keys[e] == T) {
+        if (qx < need && gx + qx < (uint32_t)k) out[gx + qx] = (int32_t)i;
+        ++qx;
+      }
+    }
+    gt_run += total >> 16;
+    eq_run += total & 0xFFFFu;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream) {
+  hipLaunchKernelGGL(k_select, dim3((unsigned)segments, (unsigned)a.bt.batch), dim3(kSelThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace tp

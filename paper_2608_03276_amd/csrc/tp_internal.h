@@ -1,0 +1,95 @@
+// Internal declarations shared by the C-ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "taskpress.h"
+
+namespace tp {
+
+// Batch description passed by value in kernel arguments (no device staging).
+struct BatchArgs {
+  int32_t batch;
+  int32_t pad_;
+  int64_t ctx_off[TP_MAX_BATCH + 1];
+  int64_t g_off[TP_MAX_BATCH + 1];
+};
+
+// ---------------------------------------------------------------- step 1 (guide scores)
+constexpr int kGuideThreads = 256;       // 4 waves of 64
+constexpr int kRowsPerWave = 64;         // two 32-row MFMA blocks per wave
+constexpr int kRowsPerGroup = 256;       // guide rows handled by one workgroup
+constexpr int kMacroTokens = 128;        // tokens staged in LDS per iteration
+constexpr int kChunkTokens = 2048;       // tokens of one segment per workgroup
+
+struct GuideArgs {
+  const uint16_t* q;  // bf16 [L][Hq][G_tot][d]
+  const uint16_t* k;  // bf16 [L][Hkv][N_tot][d]
+  float* s_key;       // fp32 [L][Hkv][N_tot]
+  float2* stats;      // [nchunk_max][L*Hq*G_tot]   per-chunk (max, sum) in the log2 domain
+  float* lse2;        // [L*Hq*G_tot]               log2-sum-exp2 of scaled logits per row
+  float* raw;         // [nrg_max][L*Hkv][N_tot]    per row-group sums of normalised attention
+  int32_t L, Hq, Hkv, R;
+  int64_t n_tot, g_tot;
+  float c;            // softmax_scale * log2(e)
+  float pool_inv;     // 1 / (R * pool_k)
+  int32_t pool_half;  // pool_k / 2
+  int32_t nchunk_max; // chunks of the longest sequence
+  int32_t nchunk_pad; // nchunk_max rounded up to a multiple of 8 (XCD count)
+  int32_t nrg_max;    // row groups of the largest R * G_b
+  BatchArgs bt;
+};
+
+struct GuideWorkspace {
+  size_t stats_off, lse_off, raw_off, total;
+};
+GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const int64_t* ctx_off,
+                                      const int64_t* g_off, int32_t batch);
+
+hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream);
+
+// ---------------------------------------------------------------- step 2 (V scales)
+struct QuantArgs {
+  const uint16_t* v;  // bf16 [rows][d]
+  float* scales;      // fp32 [rows]
+  uint8_t* vq;        // [rows][row_bytes] or nullptr
+  int64_t rows;       // L * Hkv * N_tot
+  int32_t qfmt, bits;
+  float qmax;
+};
+hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream);
+
+// ---------------------------------------------------------------- step 3 (select)
+struct SelectArgs {
+  const float* s_key;  // fp32 [L*Hkv][N_tot]
+  const float* scales; // fp32 [L*Hkv][N_tot]
+  float* s_buf;        // fp32 [L*Hkv][N_tot]   combined scores (s_out or workspace)
+  int32_t* kept;       // int32 [L*Hkv][K_tot]
+  int64_t n_tot, k_tot;
+  int32_t rule;
+  int32_t pad_;
+  int64_t k[TP_MAX_BATCH];
+  int64_t kept_off[TP_MAX_BATCH + 1];
+  BatchArgs bt;
+};
+hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream);
+
+// ---------------------------------------------------------------- step 4 (compaction)
+struct CompactArgs {
+  const int32_t* kept; // [L*Hkv][K_tot]
+  const uint16_t* k;   // bf16 [L*Hkv][N_tot][d]
+  const uint8_t* vq;   // [L*Hkv][N_tot][row_bytes] or nullptr
+  const float* scales; // [L*Hkv][N_tot] or nullptr
+  uint16_t* k_out;     // [L*Hkv][K_tot][d]
+  uint8_t* vq_out;
+  float* scales_out;
+  int64_t n_tot, k_tot;
+  int32_t row_bytes;
+  int32_t pad_;
+  int64_t kept_off[TP_MAX_BATCH + 1];
+  BatchArgs bt;
+};
+hipError_t launch_compact(const CompactArgs& a, int segments, int head_dim, hipStream_t stream);
+
+}  // namespace tp

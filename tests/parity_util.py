@@ -1,0 +1,163 @@
+"""Shared helpers of the GPU parity tests: seeded inputs on both sides, the oracle run on
+sampled segments, and the comparison rules.
+
+Comparison rules (the tolerance is the one the eviction path is held to):
+  scores      |gpu - oracle| <= 1e-3 * max(|oracle|, 2^-100)   (relative, floored)
+  scales, q   bit-exact
+  kept sets   exact when the oracle's k-th and (k+1)-th combined scores differ by more than
+              1e-3 relative; otherwise the GPU set has k elements, holds every index whose
+              oracle score exceeds T_k (1 + 1e-3) and none below T_k (1 - 1e-3)
+  compaction  bit-exact gather of the inputs at the GPU's own kept indices
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import synth
+from oracle import taskpress_oracle as o
+from paper_2608_03276_amd import binding as B
+
+RTOL = 1e-3
+FLOOR = 2.0 ** -100
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def device_inputs(w, device="cuda"):
+    """Q/K/V of workload `w` drawn on the GPU (bit-identical to the host generator)."""
+    lens = list(w.ctx_lens)
+    glens = list(w.guide_lens)
+    q = torch.empty(w.L * w.Hq * w.g_tot * w.d, dtype=torch.bfloat16, device=device)
+    k = torch.empty(w.L * w.Hkv * w.n_tot * w.d, dtype=torch.bfloat16, device=device)
+    v = torch.empty_like(k)
+    s = torch.cuda.current_stream().cuda_stream
+    synth.device_fill(q.data_ptr(), w.q, w.L, w.Hq, glens, w.d, s)
+    synth.device_fill(k.data_ptr(), w.k, w.L, w.Hkv, lens, w.d, s)
+    synth.device_fill(v.data_ptr(), w.v, w.L, w.Hkv, lens, w.d, s)
+    return q, k, v
+
+
+def host_segment(w, b, l, h):
+    """bf16 bits of the oracle's inputs for segment (b, l, h): q_group [R, G_b, d], k, v [N_b, d]."""
+    n, g = w.ctx_lens[b], w.guide_lens[b]
+    qg = np.stack([synth.rows(w.q, b, l, h * w.R + r, g, w.d) for r in range(w.R)])
+    k = synth.rows(w.k, b, l, h, n, w.d)
+    v = synth.rows(w.v, b, l, h, n, w.d)
+    return qg, k, v
+
+
+def run_gpu(w, q, k, v, rule=None, bufs=None):
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    out = B.evict(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                  rule=w.rule if rule is None else rule, keep_ratio=w.keep_ratio or 0.0,
+                  keep_budget=w.keep_budget or 0, bufs=bufs)
+    torch.cuda.synchronize()
+    return out
+
+
+def oracle_segment(w, b, l, h, rule=None):
+    qg, kb, vb = host_segment(w, b, l, h)
+    k = o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget)
+    res = o.evict_segment(qg, kb, vb, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                          rule=w.rule if rule is None else rule, k=k)
+    res["k_bits"] = kb
+    res["k"] = k
+    return res
+
+
+def seg_slice(w, bufs, b, l, h):
+    """Views of the GPU outputs of segment (b, l, h), copied to the host."""
+    n0, n1 = w.ctx_offsets()[b], w.ctx_offsets()[b + 1]
+    seg = l * w.Hkv + h
+    ko = bufs.kept_offsets
+    kt = ko[-1]
+    rb = B.row_bytes(w.qfmt, w.bits, w.d)
+    base = seg * w.n_tot
+    out = dict(
+        s_key=bufs.s_key[base + n0:base + n1].cpu().numpy(),
+        gamma=bufs.scales[base + n0:base + n1].cpu().numpy(),
+        vq=bufs.v_q[(base + n0) * rb:(base + n1) * rb].cpu().numpy().reshape(n1 - n0, rb),
+        S=bufs.s_comb[base + n0:base + n1].cpu().numpy(),
+        idx=bufs.kept_idx[seg * kt + ko[b]:seg * kt + ko[b + 1]].cpu().numpy(),
+        k_c=bufs.k_c.view(torch.int16)[(seg * kt + ko[b]) * w.d:(seg * kt + ko[b + 1]) * w.d].cpu().numpy()
+        .view(np.uint16).reshape(-1, w.d),
+        vq_c=bufs.v_q_c[(seg * kt + ko[b]) * rb:(seg * kt + ko[b + 1]) * rb].cpu().numpy().reshape(-1, rb),
+        gamma_c=bufs.scales_c[seg * kt + ko[b]:seg * kt + ko[b + 1]].cpu().numpy(),
+    )
+    return out
+
+
+def assert_scores_close(gpu, ref, what):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(gpu - ref)
+    tol = RTOL * np.maximum(np.abs(ref), FLOOR)
+    bad = np.nonzero(~(err <= tol))[0]
+    if len(bad):
+        i = bad[np.argmax(err[bad] / tol[bad])]
+        raise AssertionError(f"{what}: {len(bad)} of {len(ref)} outside 1e-3 (worst i={i}: gpu={gpu[i]!r} "
+                             f"oracle={ref[i]!r})")
+    return float(np.max(err / np.maximum(np.abs(ref), FLOOR))) if len(ref) else 0.0
+
+
+def assert_keep_set(gpu_idx, S_oracle, k, what):
+    """Rule for kept sets, with the oracle's fp32 combined scores."""
+    gpu_idx = np.asarray(gpu_idx, dtype=np.int64)
+    assert len(gpu_idx) == k, f"{what}: {len(gpu_idx)} kept, expected {k}"
+    assert np.all(np.diff(gpu_idx) > 0), f"{what}: kept indices not strictly ascending"
+    S = np.asarray(S_oracle, dtype=np.float64)
+    ref = o.select(S_oracle, k)
+    order = np.sort(S)[::-1]
+    tk = order[k - 1]
+    tk1 = order[k] if k < len(S) else -np.inf
+    if abs(tk - tk1) > RTOL * abs(tk):
+        if not np.array_equal(gpu_idx, ref):
+            diff = np.setxor1d(gpu_idx, ref)
+            raise AssertionError(f"{what}: kept set differs from the oracle at {len(diff)} indices "
+                                 f"(T_k={tk!r}, T_k+1={tk1!r}, first {diff[:8]})")
+        return 0
+    sel = np.zeros(len(S), bool)
+    sel[gpu_idx] = True
+    must = S > tk * (1 + RTOL)
+    never = S < tk * (1 - RTOL)
+    assert np.all(sel[must]), f"{what}: an index above the tie band was evicted"
+    assert not np.any(sel[never]), f"{what}: an index below the tie band was kept"
+    return int(np.setxor1d(gpu_idx, ref).size)
+
+
+def assert_topk_of_own_scores(gpu_idx, gpu_S, what):
+    """The GPU's kept set is the top-k of its own combined scores, ties to the lower index."""
+    S = np.asarray(gpu_S)
+    sel = np.zeros(len(S), bool)
+    sel[np.asarray(gpu_idx, dtype=np.int64)] = True
+    if sel.all() or not sel.any():
+        return
+    t = S[sel].min()
+    assert S[~sel].max() <= t, f"{what}: an evicted token outscores a kept one"
+    kept_at_t = np.nonzero(sel & (S == t))[0]
+    evicted_at_t = np.nonzero(~sel & (S == t))[0]
+    if len(kept_at_t) and len(evicted_at_t):
+        assert kept_at_t.max() < evicted_at_t.min(), f"{what}: tie not broken towards the lower index"
+
+
+def check_segment(w, bufs, b, l, h, ref=None, rule=None):
+    """Every output of segment (b, l, h) against the oracle; returns diagnostics."""
+    if ref is None:
+        ref = oracle_segment(w, b, l, h, rule)
+    g = seg_slice(w, bufs, b, l, h)
+    tag = f"{w.name} seg(b={b},l={l},h={h})"
+    err_s = assert_scores_close(g["s_key"], ref["s_key"], tag + " s_key")
+    assert np.array_equal(g["gamma"].view(np.uint32), ref["gamma"].view(np.uint32)), tag + " scales differ"
+    assert np.array_equal(g["vq"], ref["vq"]), tag + " quantised V differs"
+    err_S = assert_scores_close(g["S"], ref["S"].astype(np.float64), tag + " combined score")
+    band = assert_keep_set(g["idx"], ref["S"], ref["k"], tag + " kept set")
+    assert_topk_of_own_scores(g["idx"], g["S"], tag)
+    idx = g["idx"].astype(np.int64)
+    assert np.array_equal(g["k_c"], ref["k_bits"][idx]), tag + " compact K differs"
+    assert np.array_equal(g["vq_c"], ref["vq"][idx]), tag + " compact V differs"
+    assert np.array_equal(g["gamma_c"].view(np.uint32), ref["gamma"][idx].view(np.uint32)), tag + " compact scales"
+    return dict(max_rel_s_key=err_s, max_rel_S=err_S, band_mismatch=band)

@@ -1,0 +1,155 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and its host-only
+helpers and argument validation behave as documented.  No kernel is launched: every call
+below fails validation before any HIP call (the tests skip where a GPU is visible, so a
+validation bug can never turn into a launch with a fake pointer)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import taskpress_oracle as o
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "taskpress.h")
+
+from paper_2608_03276_amd import binding as B  # noqa: E402
+
+lib = B.load()
+no_gpu = pytest.mark.skipif(torch.cuda.device_count() > 0, reason="validation cases use fake device pointers")
+FAKE = 0x10000  # 16-byte aligned, never dereferenced
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tp_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in B.tp_version()
+    for s, name in B._STATUS_NAMES.items():
+        assert lib.tp_status_string(s).decode() == name
+
+
+def test_keep_count_matches_oracle():
+    rng = np.random.default_rng(3)
+    for _ in range(2000):
+        n = int(rng.integers(1, 300000))
+        r = float(rng.choice([rng.random(), 0.1, 0.2, 0.25, 0.05, 1.0, 1e-7]))
+        if r > 0:
+            assert B.tp_keep_count(n, r, 0) == o.keep_count(n, keep_ratio=r)
+        bud = int(rng.integers(1, 5000))
+        assert B.tp_keep_count(n, 0.0, bud) == o.keep_count(n, keep_budget=bud)
+    assert B.tp_keep_count(10, 0.5, 3) == -1  # both given
+    assert B.tp_keep_count(10, 0.0, 0) == -1  # neither
+    assert B.tp_keep_count(10, 1.5, 0) == -1
+    assert B.tp_keep_count(0, 0.5, 0) == -1
+
+
+def test_workspace_size():
+    d = B.dims(32, 32, 8, 128)
+    bt = B.Batch([0, 131072], [0, 64])
+    ws = B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, d, bt)
+    nch, rows = 131072 // 2048, 32 * 32 * 64
+    assert ws >= nch * rows * 8 + rows * 4 + 32 * 8 * 131072 * 4
+    assert B.tp_workspace_size(B.TP_FN_COMBINE_SELECT_TOPK, d, bt) >= 32 * 8 * 131072 * 4
+    with pytest.raises(B.TaskPressError) as e:
+        B.tp_workspace_size(7, d, bt)
+    assert e.value.status == B.TP_ERR_PARAM
+
+
+def _gs(d, bt, q=FAKE, k=FAKE, scale=0.125, pool=5, s=FAKE, ws=FAKE, wsb=1 << 40):
+    return lib.tp_guide_scores(ctypes.byref(d), ctypes.byref(bt.c) if bt is not None else None, q, k, scale, pool,
+                               s, ws, wsb, None)
+
+
+@no_gpu
+def test_guide_scores_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300], [0, 16, 20])
+    cases = [
+        (dict(q=None), B.TP_ERR_NULL),
+        (dict(k=None), B.TP_ERR_NULL),
+        (dict(s=None), B.TP_ERR_NULL),
+        (dict(scale=0.0), B.TP_ERR_PARAM),
+        (dict(scale=-1.0), B.TP_ERR_PARAM),
+        (dict(scale=float("inf")), B.TP_ERR_PARAM),
+        (dict(pool=4), B.TP_ERR_PARAM),
+        (dict(pool=0), B.TP_ERR_PARAM),
+        (dict(ws=None), B.TP_ERR_WORKSPACE),
+        (dict(wsb=100), B.TP_ERR_WORKSPACE),
+        (dict(ws=FAKE + 16), B.TP_ERR_WORKSPACE),
+        (dict(q=FAKE + 2), B.TP_ERR_PARAM),
+    ]
+    for kw, want in cases:
+        assert _gs(d, bt, **kw) == want, kw
+        assert lib.tp_last_error().decode() != ""
+    assert _gs(B.dims(2, 8, 3, 64), bt) == B.TP_ERR_SHAPE  # Hq % Hkv
+    assert _gs(B.dims(2, 8, 2, 96), bt) == B.TP_ERR_UNSUPPORTED  # head_dim
+    assert _gs(B.dims(0, 8, 2, 64), bt) == B.TP_ERR_SHAPE
+    assert _gs(d, B.Batch([0, 100, 100], [0, 16, 20])) == B.TP_ERR_SHAPE  # empty sequence
+    assert _gs(d, B.Batch([0, 100, 300], [0, 16, 16])) == B.TP_ERR_SHAPE  # empty guide
+    assert _gs(d, B.Batch([1, 100, 300], [0, 16, 20])) == B.TP_ERR_SHAPE
+    assert _gs(d, B.Batch([0, 100, 300])) == B.TP_ERR_NULL  # no guide offsets
+    assert _gs(d, B.Batch(list(range(0, 66)), list(range(0, 66)))) == B.TP_ERR_UNSUPPORTED  # batch > 64
+    assert lib.tp_guide_scores(None, ctypes.byref(bt.c), FAKE, FAKE, 0.1, 1, FAKE, FAKE, 1 << 40, None) == B.TP_ERR_NULL
+
+
+@no_gpu
+def test_quantize_validation():
+    d = B.dims(2, 8, 2, 128)
+    bt = B.Batch([0, 100])
+    q = lambda fmt=0, bits=8, v=FAKE, s=FAKE, vq=FAKE: lib.tp_quantize_v_scales(
+        ctypes.byref(d), ctypes.byref(bt.c), v, fmt, bits, s, vq, None)
+    assert q(bits=1) == B.TP_ERR_PARAM
+    assert q(bits=9) == B.TP_ERR_PARAM
+    assert q(fmt=5) == B.TP_ERR_PARAM
+    assert q(v=None) == B.TP_ERR_NULL
+    assert q(s=None) == B.TP_ERR_NULL
+    assert q(vq=FAKE + 4) == B.TP_ERR_PARAM
+
+
+@no_gpu
+def test_select_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300])
+    good = B.kept_offsets_for(bt, 0.25, 0)
+
+    def sel(rule=0, ratio=0.25, budget=0, ko=good, kept=FAKE, s_out=FAKE, ws=None, wsb=0):
+        return lib.tp_combine_select_topk(ctypes.byref(d), ctypes.byref(bt.c), FAKE, FAKE, rule, ratio, budget,
+                                          B._i64_array(ko), kept, s_out, ws, wsb, None)
+
+    assert sel(rule=4) == B.TP_ERR_PARAM
+    assert sel(ratio=0.25, budget=10) == B.TP_ERR_PARAM
+    assert sel(ratio=0.0, budget=0) == B.TP_ERR_PARAM
+    assert sel(ratio=1.5) == B.TP_ERR_PARAM
+    assert sel(ko=[0, 25, 74]) == B.TP_ERR_SHAPE
+    assert sel(ko=[1, 26, 76]) == B.TP_ERR_SHAPE
+    assert sel(kept=None) == B.TP_ERR_NULL
+    assert sel(s_out=None) == B.TP_ERR_WORKSPACE  # no s_out and no workspace
+
+
+@no_gpu
+def test_compact_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300])
+
+    def cp(ko=(0, 25, 75), vq=FAKE, vqo=FAKE, sc=FAKE, sco=FAKE, fmt=0, bits=8):
+        return lib.tp_compact_kv(ctypes.byref(d), ctypes.byref(bt.c), B._i64_array(ko), FAKE, FAKE, vq, sc, fmt, bits,
+                                 FAKE, vqo, sco, None)
+
+    assert cp(ko=(0, 101, 150)) == B.TP_ERR_SHAPE  # more kept than tokens
+    assert cp(ko=(0, 30, 20)) == B.TP_ERR_SHAPE
+    assert cp(vq=None) == B.TP_ERR_NULL
+    assert cp(sco=None) == B.TP_ERR_NULL
+    assert cp(bits=0) == B.TP_ERR_PARAM

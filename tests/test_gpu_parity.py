@@ -1,0 +1,272 @@
+"""GPU path (through the C ABI) against the CPU oracle on the same seeded inputs.
+
+Sizes span several tiles and ragged tails; the full-size workloads are checked on sampled
+segments in test_gpu_fullsize.py.  Rules: see parity_util."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import taskpress_oracle as o
+from paper_2608_03276_amd import binding as B
+from synth import workloads as W
+
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_tensor(bits: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+# ----------------------------------------------------------------------------- generator
+def test_device_generator_matches_host(gpu_lib):
+    for s, L, H, lens, d in [(synth.Stream(11, synth.TAG_K), 2, 3, [5, 300, 1], 64),
+                             (synth.Stream(12, synth.TAG_V, synth.DIST_STUDENT_T3, 0.01, 30.0), 1, 2, [2000, 777], 128)]:
+        pu.log(f"generator {s} L={L} H={H} lens={lens} d={d}")
+        t = torch.empty(L * H * sum(lens) * d, dtype=torch.bfloat16, device="cuda")
+        synth.device_fill(t.data_ptr(), s, L, H, lens, d, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        host = synth.host_tensor(s, L, H, lens, d).reshape(-1)
+        assert np.array_equal(t.view(torch.int16).cpu().numpy().view(np.uint16), host)
+
+
+# ----------------------------------------------------------------------------- step 2
+def _run_quant(vbits, L, Hkv, lens, d, qfmt, bits, with_vq=True):
+    dd = B.dims(L, Hkv, Hkv, d)
+    bt = B.Batch(np.concatenate([[0], np.cumsum(lens)]).tolist())
+    v = _bf16_tensor(vbits.reshape(-1))
+    n = L * Hkv * sum(lens)
+    scales = torch.empty(n, dtype=torch.float32, device="cuda")
+    vq = torch.empty(n * B.row_bytes(qfmt, bits, d), dtype=torch.uint8, device="cuda") if with_vq else None
+    B.tp_quantize_v_scales(dd, bt, v, qfmt, bits, scales, vq)
+    torch.cuda.synchronize()
+    return scales.cpu().numpy(), None if vq is None else vq.cpu().numpy()
+
+
+@pytest.mark.parametrize("qfmt,bits,d", [(0, 8, 128), (0, 8, 64), (0, 4, 128), (0, 4, 64), (0, 2, 128), (0, 6, 64),
+                                         (1, 8, 128), (1, 8, 64)])
+def test_quantize_parity(gpu_lib, qfmt, bits, d):
+    pu.log(f"quantize qfmt={qfmt} bits={bits} d={d}")
+    L, Hkv, lens = 2, 3, [1, 33, 1000]
+    s = synth.Stream(21, synth.TAG_V, synth.DIST_STUDENT_T3, 0.02, 50.0)
+    vb = synth.host_tensor(s, L, Hkv, lens, d)
+    vb[0, 1, 5] = 0          # all-zero row
+    vb[1, 2, 7] = 0x8000     # all -0.0 row
+    vb[1, 0, 9, :3] = [0x7F7F, 0xFF7F, 0x0001]  # largest finite bf16 and a subnormal
+    g, q = _run_quant(vb, L, Hkv, lens, d, qfmt, bits)
+    rows = o.bf16_to_f64(vb.reshape(-1, d))
+    gr = o.value_scales(rows, qfmt, bits)
+    qr = o.pack_codes(o.quantize_values(rows, gr, qfmt, bits), qfmt, bits)
+    assert np.array_equal(g.view(np.uint32), gr.view(np.uint32))
+    assert np.array_equal(q.reshape(qr.shape), qr)
+    g2, _ = _run_quant(vb, L, Hkv, lens, d, qfmt, bits, with_vq=False)
+    assert np.array_equal(g2.view(np.uint32), gr.view(np.uint32))
+
+
+@pytest.mark.parametrize("qfmt,bits", [(0, 8), (0, 4), (1, 8)])
+def test_quantize_every_bf16_absmax(gpu_lib, qfmt, bits):
+    """Every positive finite bf16 as a row's absmax, with 127 random values of smaller magnitude."""
+    pu.log(f"quantize exhaustive absmax qfmt={qfmt} bits={bits}")
+    rng = np.random.default_rng(31)
+    amax = np.arange(1, 0x7F80, dtype=np.uint16)
+    n = len(amax)
+    mags = (rng.random((n, 127)) * (amax[:, None].astype(np.float64) + 1)).astype(np.uint16)
+    signs = (rng.random((n, 127)) < 0.5).astype(np.uint16) << 15
+    rows = np.concatenate([amax[:, None] | ((rng.random((n, 1)) < 0.5).astype(np.uint16) << 15), mags | signs], axis=1)
+    for i in range(n):  # move the absmax element around
+        j = i % 128
+        rows[i, 0], rows[i, j] = rows[i, j], rows[i, 0]
+    g, q = _run_quant(rows, 1, 1, [n], 128, qfmt, bits)
+    vals = o.bf16_to_f64(rows)
+    gr = o.value_scales(vals, qfmt, bits)
+    qr = o.pack_codes(o.quantize_values(vals, gr, qfmt, bits), qfmt, bits)
+    assert np.array_equal(g.view(np.uint32), gr.view(np.uint32))
+    bad = np.nonzero(np.any(q.reshape(qr.shape) != qr, axis=1))[0]
+    assert len(bad) == 0, f"{len(bad)} rows differ, first absmax bits {hex(int(amax[bad[0]]))}"
+
+
+# ----------------------------------------------------------------------------- step 4
+@pytest.mark.parametrize("qfmt,bits,d", [(0, 8, 128), (0, 4, 64), (1, 8, 64)])
+def test_compact_parity(gpu_lib, qfmt, bits, d):
+    pu.log(f"compact qfmt={qfmt} bits={bits} d={d}")
+    rng = np.random.default_rng(41)
+    L, Hkv, lens = 2, 2, [7, 300, 1]
+    kept = [3, 41, 1]
+    ntot, kt = sum(lens), sum(kept)
+    rb = B.row_bytes(qfmt, bits, d)
+    kb = rng.integers(0, 2 ** 16, (L * Hkv, ntot, d), dtype=np.uint16)
+    vq = rng.integers(0, 256, (L * Hkv, ntot, rb), dtype=np.uint8)
+    sc = rng.random((L * Hkv, ntot)).astype(np.float32)
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    ko = np.concatenate([[0], np.cumsum(kept)])
+    idx = np.zeros((L * Hkv, kt), dtype=np.int32)
+    for s in range(L * Hkv):
+        for b in range(len(lens)):
+            idx[s, ko[b]:ko[b + 1]] = np.sort(rng.choice(lens[b], kept[b], replace=False))
+    idx[1, 5] = -1            # out of range -> zero row
+    idx[2, 10] = lens[1]      # out of range -> zero row
+    dd = B.dims(L, Hkv, Hkv, d)
+    bt = B.Batch(offs.tolist())
+    k_out = torch.empty(L * Hkv * kt * d, dtype=torch.bfloat16, device="cuda")
+    vq_out = torch.empty(L * Hkv * kt * rb, dtype=torch.uint8, device="cuda")
+    sc_out = torch.empty(L * Hkv * kt, dtype=torch.float32, device="cuda")
+    B.tp_compact_kv(dd, bt, ko.tolist(), torch.from_numpy(idx).cuda(), _bf16_tensor(kb), torch.from_numpy(vq).cuda(),
+                    torch.from_numpy(sc).cuda(), qfmt, bits, k_out, vq_out, sc_out)
+    torch.cuda.synchronize()
+    ko_ = k_out.view(torch.int16).cpu().numpy().view(np.uint16).reshape(L * Hkv, kt, d)
+    vo = vq_out.cpu().numpy().reshape(L * Hkv, kt, rb)
+    so = sc_out.cpu().numpy().reshape(L * Hkv, kt)
+    for s in range(L * Hkv):
+        for b in range(len(lens)):
+            for t in range(ko[b], ko[b + 1]):
+                i = idx[s, t]
+                if 0 <= i < lens[b]:
+                    src = offs[b] + i
+                    assert np.array_equal(ko_[s, t], kb[s, src]) and np.array_equal(vo[s, t], vq[s, src])
+                    assert so[s, t] == sc[s, src]
+                else:
+                    assert not ko_[s, t].any() and not vo[s, t].any() and so[s, t] == 0
+
+
+# ----------------------------------------------------------------------------- step 3
+def _select_inputs(rng, L, Hkv, lens, tie_levels):
+    n = L * Hkv * sum(lens)
+    if tie_levels:
+        sk = (rng.integers(0, tie_levels, n).astype(np.float32) * np.float32(0.125)).astype(np.float32)
+        g = (rng.integers(1, 4, n).astype(np.float32) * np.float32(0.5)).astype(np.float32)
+    else:
+        sk = (rng.random(n) * 10.0 ** rng.integers(-30, 1, n)).astype(np.float32)
+        g = (rng.random(n) * 10.0 ** rng.integers(-3, 1, n)).astype(np.float32)
+    return sk, g
+
+
+@pytest.mark.parametrize("rule", [0, 1, 2, 3])
+@pytest.mark.parametrize("ties", [0, 5])
+def test_select_parity(gpu_lib, rule, ties):
+    pu.log(f"select rule={rule} ties={ties}")
+    rng = np.random.default_rng(51 + rule + ties)
+    L, Hkv, lens = 2, 3, [1, 5, 1000, 4099, 70000]
+    for ratio, budget in [(0.1, 0), (1.0, 0), (0.0, 100), (0.0, 1)]:
+        sk, g = _select_inputs(rng, L, Hkv, lens, ties)
+        dd = B.dims(L, Hkv, Hkv, 64)
+        bt = B.Batch(np.concatenate([[0], np.cumsum(lens)]).tolist())
+        ko = B.kept_offsets_for(bt, ratio, budget)
+        kt = ko[-1]
+        kept = torch.empty(L * Hkv * kt, dtype=torch.int32, device="cuda")
+        s_out = torch.empty(L * Hkv * sum(lens), dtype=torch.float32, device="cuda")
+        B.tp_combine_select_topk(dd, bt, torch.from_numpy(sk).cuda(), torch.from_numpy(g).cuda(), rule, ratio,
+                                 budget, ko, kept, s_out)
+        torch.cuda.synchronize()
+        kept_h = kept.cpu().numpy().reshape(L * Hkv, kt)
+        S_h = s_out.cpu().numpy().reshape(L * Hkv, -1)
+        skr, gr = sk.reshape(L * Hkv, -1), g.reshape(L * Hkv, -1)
+        offs = bt.ctx_offsets
+        for s in range(L * Hkv):
+            for b in range(len(lens)):
+                a, e = offs[b], offs[b + 1]
+                S_ref = o.combine(skr[s, a:e], gr[s, a:e], rule)
+                k = o.keep_count(lens[b], ratio or None, budget or None)
+                got = kept_h[s, ko[b]:ko[b + 1]]
+                tag = f"rule={rule} seg={s} b={b}"
+                if rule == o.COMBINE_NORM_ADD:  # norms are sums in a different order: tolerance rules
+                    pu.assert_scores_close(S_h[s, a:e], S_ref.astype(np.float64), tag)
+                    pu.assert_keep_set(got, S_ref, k, tag)
+                    pu.assert_topk_of_own_scores(got, S_h[s, a:e], tag)
+                else:  # identical fp32 inputs: bit-exact
+                    assert np.array_equal(S_h[s, a:e].view(np.uint32), S_ref.view(np.uint32)), tag
+                    assert np.array_equal(got, o.select(S_ref, k)), tag
+
+
+def test_select_all_equal_and_zero(gpu_lib):
+    for val in [0.0, 1.5]:
+        n = 5000
+        sk = np.full(n, val, np.float32)
+        g = np.ones(n, np.float32)
+        dd = B.dims(1, 1, 1, 64)
+        bt = B.Batch([0, n])
+        ko = B.kept_offsets_for(bt, 0.3, 0)
+        kept = torch.empty(ko[-1], dtype=torch.int32, device="cuda")
+        B.tp_combine_select_topk(dd, bt, torch.from_numpy(sk).cuda(), torch.from_numpy(g).cuda(), 0, 0.3, 0, ko,
+                                 kept, torch.empty(n, dtype=torch.float32, device="cuda"))
+        torch.cuda.synchronize()
+        assert np.array_equal(kept.cpu().numpy(), np.arange(ko[-1]))
+
+
+# ----------------------------------------------------------------------------- step 1
+GUIDE_CASES = [
+    # (name, L, Hq, Hkv, d, lens, glens, k-dist, pool)
+    ("tiny-like", 1, 8, 2, 64, [1024], [16], synth.DIST_NORMAL, 5),
+    ("ragged-d128", 2, 8, 2, 128, [1, 31, 32, 33, 2047, 2048, 2049, 5000], [1, 3, 64, 64, 100, 7, 64, 128],
+     synth.DIST_NORMAL, 5),
+    ("two-row-groups", 1, 16, 2, 128, [3000, 700], [40, 33], synth.DIST_NORMAL, 3),
+    ("mha-g1-pool1", 1, 4, 4, 64, [777], [1], synth.DIST_NORMAL, 1),
+    ("heavy-tail-outliers", 1, 8, 2, 128, [4500], [64], synth.DIST_STUDENT_T3, 7),
+    ("pool-wider-than-seq", 1, 2, 1, 64, [1, 2, 3], [2, 1, 5], synth.DIST_NORMAL, 9),
+]
+
+
+@pytest.mark.parametrize("case", GUIDE_CASES, ids=[c[0] for c in GUIDE_CASES])
+def test_guide_scores_parity(gpu_lib, case):
+    name, L, Hq, Hkv, d, lens, glens, dist, pool = case
+    pu.log(f"guide scores case {name}")
+    out_frac, out_scale = (0.02, 30.0) if dist == synth.DIST_STUDENT_T3 else (0.0, 1.0)
+    w = W.Workload(name, L, Hq, Hkv, d, tuple(lens), tuple(glens), synth.Stream(61, synth.TAG_Q),
+                   synth.Stream(61, synth.TAG_K, dist, out_frac, out_scale), synth.Stream(61, synth.TAG_V),
+                   keep_ratio=0.25, pool_k=pool)
+    q, k, v = pu.device_inputs(w)
+    dd = B.dims(L, Hq, Hkv, d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    s_key = torch.empty(L * Hkv * w.n_tot, dtype=torch.float32, device="cuda")
+    ws = torch.empty(B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, dd, bt), dtype=torch.uint8, device="cuda")
+    B.tp_guide_scores(dd, bt, q, k, w.softmax_scale, pool, s_key, ws)
+    torch.cuda.synchronize()
+    got = s_key.cpu().numpy().reshape(L * Hkv, w.n_tot)
+    offs = w.ctx_offsets()
+    worst = 0.0
+    for b in range(w.batch):
+        for l in range(L):
+            for h in range(Hkv):
+                qg, kb, _ = pu.host_segment(w, b, l, h)
+                ref = o.key_scores(o.bf16_to_f64(qg), o.bf16_to_f64(kb), w.softmax_scale, pool)
+                worst = max(worst, pu.assert_scores_close(got[l * Hkv + h, offs[b]:offs[b + 1]], ref,
+                                                          f"{name} b={b} l={l} h={h}"))
+    pu.log(f"  max rel err {worst:.3g}")
+
+
+# ----------------------------------------------------------------------------- whole path
+@pytest.mark.parametrize("rule", [0, 3])
+def test_end_to_end_tiny(gpu_lib, rule):
+    w = W.tiny()
+    pu.log(f"end-to-end {w.describe()} rule={rule}")
+    q, k, v = pu.device_inputs(w)
+    bufs = pu.run_gpu(w, q, k, v, rule=rule)
+    for l in range(w.L):
+        for h in range(w.Hkv):
+            pu.check_segment(w, bufs, 0, l, h, rule=rule)
+
+
+def test_end_to_end_ragged_int4_fp8(gpu_lib):
+    base = W.ragged8()
+    for qfmt, bits in [(0, 4), (1, 8)]:
+        w = base.with_(name=f"ragged-small-{qfmt}-{bits}", L=2, ctx_lens=(3000, 1, 4097, 800),
+                       guide_lens=(32, 128, 5, 64), keep_budget=700, qfmt=qfmt, bits=bits)
+        pu.log(f"end-to-end {w.describe()}")
+        q, k, v = pu.device_inputs(w)
+        bufs = pu.run_gpu(w, q, k, v)
+        for b in range(w.batch):
+            for l in range(w.L):
+                for h in (0, w.Hkv - 1):
+                    pu.check_segment(w, bufs, b, l, h)
+
+
+def test_deterministic(gpu_lib):
+    w = W.llama8b_32k().with_(name="det", L=2, ctx_lens=(9000, 5001), guide_lens=(64, 17))
+    q, k, v = pu.device_inputs(w)
+    a = pu.run_gpu(w, q, k, v)
+    snap = {n: getattr(a, n).clone() for n in ("s_key", "scales", "v_q", "s_comb", "kept_idx", "k_c", "v_q_c",
+                                               "scales_c")}
+    b = pu.run_gpu(w, q, k, v)
+    for n, t in snap.items():
+        assert torch.equal(t.view(torch.uint8), getattr(b, n).view(torch.uint8)), n
