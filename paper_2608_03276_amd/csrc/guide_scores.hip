@@ -15,8 +15,10 @@
 // the lane); pass 2 swaps the operands, so each lane owns one token and 16 rows (the
 // token's sum over rows reduces inside the lane).  The same register fragments serve both
 // orientations because the A and B operand layouts of the instruction coincide.  K is
-// streamed through LDS in 128-token tiles (double-buffered through registers); the guide
-// queries of a wave stay in registers for its whole chunk.
+// streamed HBM -> LDS in 128-token tiles with direct global-to-LDS loads (double-buffered,
+// XOR-swizzled); the guide queries of a wave stay in registers for its whole chunk.  Each
+// wave software-pipelines its 32x32 units: the MFMA chain of unit u+1 is interleaved with
+// the exp/add work of unit u, so the matrix core and the vector ALU run concurrently.
 #include "tp_internal.h"
 
 namespace tp {
@@ -33,11 +35,11 @@ union Frag {
 template <int D>
 struct Cfg {
   static constexpr int kSteps = D / 16;                     // MFMA k-steps over d
-  static constexpr int kHalf = D / 2;                       // d columns per half-wave
-  static constexpr int kStride = D + 8;                     // LDS row pitch (bf16), +16 B pad
   static constexpr int kPieces = D / 8;                     // 16-byte pieces per token row
-  static constexpr int kLoads = kMacroTokens * kPieces / kGuideThreads;
-  static_assert(kLoads * kGuideThreads == kMacroTokens * kPieces, "tile split");
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kTileBytes = kMacroTokens * kRowBytes;
+  static constexpr int kRowsPerLoad = 1024 / kRowBytes;     // token rows one wave-wide 16 B load fills
+  static constexpr int kLoadsPerWave = kTileBytes / 1024 / 4;
 };
 
 struct Work {
@@ -45,6 +47,8 @@ struct Work {
   int64_t n0, nb, c0, c1, g0;
   int gb, rows, row0, nrows;
 };
+
+__device__ inline int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Workgroup -> (row group, chunk, segment, sequence).  Consecutive workgroup ids are dealt
 // round-robin to the 8 XCDs; the row groups of one chunk are given ids 8 apart so they land
@@ -79,20 +83,6 @@ __device__ inline int64_t grow_of(const GuideArgs& a, const Work& w, int rho) {
   return ((int64_t)w.l * a.Hq + qh) * a.g_tot + w.g0 + j;
 }
 
-// Wave layout: WR waves split the rows (64 each), WT = 4/WR teams split the 4 sub-tiles.
-struct WaveRole {
-  int wr, wt, WR, WT;
-};
-__device__ inline WaveRole wave_role(const Work& w) {
-  WaveRole r;
-  r.WR = w.nrows > 128 ? 4 : (w.nrows > 64 ? 2 : 1);
-  r.WT = 4 / r.WR;
-  const int wave = threadIdx.x >> 6;
-  r.wr = wave % r.WR;
-  r.wt = wave / r.WR;
-  return r;
-}
-
 template <int D>
 __device__ inline void load_q(const GuideArgs& a, const Work& w, int wrow0, Frag (&qf)[2][Cfg<D>::kSteps]) {
   const int lane = threadIdx.x & 63;
@@ -100,7 +90,7 @@ __device__ inline void load_q(const GuideArgs& a, const Work& w, int wrow0, Frag
   for (int rb = 0; rb < 2; ++rb) {
     const int rho = wrow0 + rb * 32 + (lane & 31);
     if (rho < w.rows) {
-      const uint16_t* src = a.q + grow_of(a, w, rho) * D + (lane >> 5) * Cfg<D>::kHalf;
+      const uint16_t* src = a.q + grow_of(a, w, rho) * D + (lane >> 5) * (D / 2);
 #pragma unroll
       for (int s = 0; s < Cfg<D>::kSteps; ++s) qf[rb][s].u = *(const uint4*)(src + 8 * s);
     } else {
@@ -110,34 +100,49 @@ __device__ inline void load_q(const GuideArgs& a, const Work& w, int wrow0, Frag
   }
 }
 
+// The K tile of 128 tokens sits in LDS without padding; the 16-byte piece p of token row r
+// is stored at piece p ^ (r mod kPieces), which makes the fragment reads below conflict-free.
+// Each wave fills its share with direct global->LDS loads (64 lanes x 16 B = 1 KB per
+// instruction, lane i landing at byte 16 i).  Tokens past the chunk end re-load the last
+// valid row, so every LDS byte holds finite data and no load leaves the sequence.
 template <int D>
-__device__ inline void load_tile(const uint16_t* kseg, int64_t t0, int64_t c1, uint4 (&st)[Cfg<D>::kLoads]) {
-#pragma unroll
-  for (int j = 0; j < Cfg<D>::kLoads; ++j) {
-    const int p = threadIdx.x + j * kGuideThreads;
-    const int tok = p / Cfg<D>::kPieces, pc = p % Cfg<D>::kPieces;
-    const int64_t gt = t0 + tok;
-    st[j] = gt < c1 ? *(const uint4*)(kseg + gt * D + pc * 8) : make_uint4(0, 0, 0, 0);
-  }
-}
-
-template <int D>
-__device__ inline void store_tile(uint16_t* buf, const uint4 (&st)[Cfg<D>::kLoads]) {
-#pragma unroll
-  for (int j = 0; j < Cfg<D>::kLoads; ++j) {
-    const int p = threadIdx.x + j * kGuideThreads;
-    const int tok = p / Cfg<D>::kPieces, pc = p % Cfg<D>::kPieces;
-    *(uint4*)(buf + tok * Cfg<D>::kStride + pc * 8) = st[j];
-  }
-}
-
-// K fragment of sub-tile `st` for this lane: token st*32 + lane%32, columns of its half.
-template <int D>
-__device__ inline void read_kfrag(const uint16_t* buf, int st, Frag (&kf)[Cfg<D>::kSteps]) {
+__device__ inline void issue_tile(const uint16_t* kseg, int64_t t0, int64_t c1, char* buf, int wave) {
+  using C = Cfg<D>;
   const int lane = threadIdx.x & 63;
-  const uint16_t* src = buf + (st * 32 + (lane & 31)) * Cfg<D>::kStride + (lane >> 5) * Cfg<D>::kHalf;
+  const char* base = (const char*)(kseg + t0 * D);  // wave-uniform
+  const int last = (int)(c1 - 1 - t0);               // last valid row of this tile
 #pragma unroll
-  for (int s = 0; s < Cfg<D>::kSteps; ++s) kf[s].u = *(const uint4*)(src + 8 * s);
+  for (int j = 0; j < C::kLoadsPerWave; ++j) {
+    const int blk = wave * C::kLoadsPerWave + j;  // 1 KB block of the tile
+    int r = blk * C::kRowsPerLoad + lane / C::kPieces;
+    const int p = (lane % C::kPieces) ^ (r & (C::kPieces - 1));
+    r = r < last ? r : last;
+    __builtin_amdgcn_global_load_lds((const void*)(base + (uint32_t)(r * C::kRowBytes + p * 16)),
+                                     (__attribute__((address_space(3))) void*)(buf + blk * 1024), 16, 0, 0);
+  }
+}
+
+// K fragment of sub-tile `st` for this lane: token st*32 + lane%32, the d-columns of its
+// half-wave (lane/32), k-step s covering columns half*D/2 + 8s .. +8.
+template <int D>
+__device__ inline void read_kfrag(const char* buf, int st, Frag (&kf)[Cfg<D>::kSteps]) {
+  using C = Cfg<D>;
+  const int lane = threadIdx.x & 63;
+  const int r = st * 32 + (lane & 31);
+  const char* row = buf + r * C::kRowBytes;
+#pragma unroll
+  for (int s = 0; s < C::kSteps; ++s) {
+    const int p = (lane >> 5) * (C::kPieces / 2) + s;
+    kf[s].u = *(const uint4*)(row + ((p ^ (r & (C::kPieces - 1))) * 16));
+  }
+}
+
+template <int KS>
+__device__ inline f32x16 mfma_chain(const Frag (&a)[KS], const Frag (&b)[KS]) {
+  f32x16 acc = {};
+#pragma unroll
+  for (int s = 0; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s].v, b[s].v, acc, 0, 0, 0);
+  return acc;
 }
 
 __device__ inline void merge_stats(float& m, float& s, float m2, float s2) {
@@ -147,19 +152,95 @@ __device__ inline void merge_stats(float& m, float& s, float m2, float s2) {
   m = mn;
 }
 
+// MFMA / VALU interleave: after each MFMA of the next unit, let `n` VALU ops issue.
+template <int KS, int N>
+__device__ inline void interleave() {
+#pragma unroll
+  for (int i = 0; i < KS; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, N, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------- pass 1
+// Online (max, sum) of the scaled logits of one unit (32 tokens x 32 rows): acc[i] is the
+// logit of token (i/4)*8 + (lane/32)*4 + i%4 and row lane%32.
+template <bool PARTIAL>
+__device__ inline void stats_update(const f32x16& acc, float c, float& m, float& s, int nvalid) {
+  const int lane = threadIdx.x & 63;
+  float x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] = acc[i];
+  if (PARTIAL) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tok = (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+      x[i] = tok < nvalid ? x[i] : -INFINITY;
+    }
+  }
+  float t0 = fmaxf(fmaxf(x[0], x[1]), x[2]), t1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
+  float t2 = fmaxf(fmaxf(x[6], x[7]), x[8]), t3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
+  float t4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
+  const float tmax = fmaxf(fmaxf(fmaxf(t0, t1), x[15]), fmaxf(fmaxf(t2, t3), t4));
+  const float mn = fmaxf(m, tmax * c);
+  float e0 = 0.f, e1 = 0.f, e2 = 0.f, e3 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; i += 4) {
+    e0 += __builtin_amdgcn_exp2f(fmaf(x[i + 0], c, -mn));
+    e1 += __builtin_amdgcn_exp2f(fmaf(x[i + 1], c, -mn));
+    e2 += __builtin_amdgcn_exp2f(fmaf(x[i + 2], c, -mn));
+    e3 += __builtin_amdgcn_exp2f(fmaf(x[i + 3], c, -mn));
+  }
+  const float sn = s * __builtin_amdgcn_exp2f(m - mn) + ((e0 + e1) + (e2 + e3));
+  if (PARTIAL) {  // a lane whose tokens are all masked so far keeps (-inf, 0)
+    const bool keep = mn == -INFINITY;
+    s = keep ? s : sn;
+    m = keep ? m : mn;
+  } else {
+    s = sn;
+    m = mn;
+  }
+}
+
+template <int D, int WR, bool PARTIAL>
+__device__ inline void stats_macro(const char* buf, const Frag (&qf)[2][Cfg<D>::kSteps], float c, int wt,
+                                   int64_t t0, int64_t c1, float (&m)[2], float (&s)[2]) {
+  using C = Cfg<D>;
+  constexpr int WT = 4 / WR, SUBS = 4 / WT, UNITS = 2 * SUBS;
+  Frag kf[2][C::kSteps];
+  read_kfrag<D>(buf, wt, kf[0]);
+  f32x16 acc = mfma_chain<C::kSteps>(kf[0], qf[0]);
+#pragma unroll
+  for (int u = 0; u < UNITS; ++u) {
+    const int si = u >> 1, rb = u & 1;
+    f32x16 nxt = {};
+    if (u + 1 < UNITS) {
+      const int si1 = (u + 1) >> 1, rb1 = (u + 1) & 1;
+      if (rb == 0 && si + 1 < SUBS) read_kfrag<D>(buf, wt + (si + 1) * WT, kf[(si + 1) & 1]);
+      nxt = mfma_chain<C::kSteps>(kf[si1 & 1], qf[rb1]);
+    }
+    const int64_t sub0 = t0 + (wt + si * WT) * 32;
+    const int nvalid = c1 - sub0 >= 32 ? 32 : (c1 > sub0 ? (int)(c1 - sub0) : 0);
+    stats_update<PARTIAL>(acc, c, m[rb], s[rb], nvalid);
+    interleave<C::kSteps, 7>();
+    acc = nxt;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kGuideThreads, 2) void k_guide_stats(GuideArgs a) {
   Work w;
   if (!decode(a, w)) return;
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t kt[2][kMacroTokens * C::kStride];
+  __shared__ __attribute__((aligned(1024))) char kt[2][C::kTileBytes];
   __shared__ float2 xch[4][kRowsPerGroup];
 
   const int lane = threadIdx.x & 63;
-  const WaveRole role = wave_role(w);
-  const int wrow0 = w.row0 + role.wr * kRowsPerWave;
-  const bool blk_ok[2] = {wrow0 < w.rows, wrow0 + 32 < w.rows};
+  const int wave = uniform(threadIdx.x >> 6);
+  const int WR = w.nrows > 128 ? 4 : (w.nrows > 64 ? 2 : 1);
+  const int WT = 4 / WR;
+  const int wr = wave % WR, wt = wave / WR;
+  const int wrow0 = w.row0 + wr * kRowsPerWave;
 
   Frag qf[2][C::kSteps];
   load_q<D>(a, w, wrow0, qf);
@@ -167,51 +248,24 @@ __global__ __launch_bounds__(kGuideThreads, 2) void k_guide_stats(GuideArgs a) {
 
   const uint16_t* kseg = a.k + ((int64_t)w.seg * a.n_tot + w.n0) * D;
   const int ntiles = (int)((w.c1 - w.c0 + kMacroTokens - 1) / kMacroTokens);
-  uint4 stage[C::kLoads];
-  load_tile<D>(kseg, w.c0, w.c1, stage);
-  store_tile<D>(kt[0], stage);
+  issue_tile<D>(kseg, w.c0, w.c1, kt[0], wave);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int it = 0; it < ntiles; ++it) {
     const int64_t t0 = w.c0 + (int64_t)it * kMacroTokens;
-    if (it + 1 < ntiles) load_tile<D>(kseg, t0 + kMacroTokens, w.c1, stage);
-    const uint16_t* buf = kt[it & 1];
-    for (int st = role.wt; st < kMacroTokens / 32; st += role.WT) {
-      const int64_t sub0 = t0 + st * 32;
-      if (sub0 >= w.c1) break;
-      const int nvalid = w.c1 - sub0 < 32 ? (int)(w.c1 - sub0) : 32;
-      Frag kf[C::kSteps];
-      read_kfrag<D>(buf, st, kf);
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        if (!blk_ok[rb]) continue;
-        f32x16 acc = {};
-#pragma unroll
-        for (int ks = 0; ks < C::kSteps; ++ks)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks].v, qf[rb][ks].v, acc, 0, 0, 0);
-        // acc[i] = <k_token, q_row>, token = (i/4)*8 + (lane/32)*4 + i%4, row = lane%32
-        if (nvalid < 32) {
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int tok = (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-            if (tok >= nvalid) acc[i] = -INFINITY;
-          }
-        }
-        float tmax = acc[0];
-#pragma unroll
-        for (int i = 1; i < 16; ++i) tmax = fmaxf(tmax, acc[i]);
-        const float mn = fmaxf(m[rb], tmax * a.c);
-        float sum = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sum += __builtin_amdgcn_exp2f(fmaf(acc[i], a.c, -mn));
-        const float sn = s[rb] * __builtin_amdgcn_exp2f(m[rb] - mn) + sum;
-        if (mn != -INFINITY) {
-          s[rb] = sn;
-          m[rb] = mn;
-        }
-      }
+    if (it + 1 < ntiles) issue_tile<D>(kseg, t0 + kMacroTokens, w.c1, kt[(it + 1) & 1], wave);
+    const char* buf = kt[it & 1];
+    if (t0 + kMacroTokens <= w.c1) {
+      if (WR == 4) stats_macro<D, 4, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
+      else if (WR == 2) stats_macro<D, 2, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
+      else stats_macro<D, 1, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
+    } else {
+      if (WR == 4) stats_macro<D, 4, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
+      else if (WR == 2) stats_macro<D, 2, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
+      else stats_macro<D, 1, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
     }
-    if (it + 1 < ntiles) store_tile<D>(kt[(it + 1) & 1], stage);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 
@@ -221,15 +275,15 @@ __global__ __launch_bounds__(kGuideThreads, 2) void k_guide_stats(GuideArgs a) {
     const float mo = __shfl_xor(m[rb], 32);
     const float so = __shfl_xor(s[rb], 32);
     merge_stats(m[rb], s[rb], mo, so);
-    if (lane < 32) xch[role.wt][role.wr * kRowsPerWave + rb * 32 + lane] = make_float2(m[rb], s[rb]);
+    if (lane < 32) xch[wt][wr * kRowsPerWave + rb * 32 + lane] = make_float2(m[rb], s[rb]);
   }
   __syncthreads();
   const int t = threadIdx.x;
-  if (t < role.WR * kRowsPerWave) {
+  if (t < WR * kRowsPerWave) {
     const int rho = w.row0 + t;
     if (rho < w.rows) {
       float mm = xch[0][t].x, ss = xch[0][t].y;
-      for (int q = 1; q < role.WT; ++q) merge_stats(mm, ss, xch[q][t].x, xch[q][t].y);
+      for (int q = 1; q < WT; ++q) merge_stats(mm, ss, xch[q][t].x, xch[q][t].y);
       const int64_t growtot = (int64_t)a.L * a.Hq * a.g_tot;
       a.stats[(int64_t)w.chunk * growtot + grow_of(a, w, rho)] = make_float2(mm, ss);
     }
@@ -259,18 +313,63 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
 }
 
 // ---------------------------------------------------------------------------- pass 2
+// Normalised weights of one unit (32 rows x 32 tokens): acc[i] is the logit of row
+// (i/4)*8 + (lane/32)*4 + i%4 and token lane%32; returns the lane's sum over its 16 rows.
+__device__ inline float attn_sum(const f32x16& acc, float c, const float (&lz)[16]) {
+  float e0 = 0.f, e1 = 0.f, e2 = 0.f, e3 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; i += 4) {
+    e0 += __builtin_amdgcn_exp2f(fmaf(acc[i + 0], c, -lz[i + 0]));
+    e1 += __builtin_amdgcn_exp2f(fmaf(acc[i + 1], c, -lz[i + 1]));
+    e2 += __builtin_amdgcn_exp2f(fmaf(acc[i + 2], c, -lz[i + 2]));
+    e3 += __builtin_amdgcn_exp2f(fmaf(acc[i + 3], c, -lz[i + 3]));
+  }
+  return (e0 + e1) + (e2 + e3);
+}
+
+template <int D, int WR>
+__device__ inline void attn_macro(const char* buf, const Frag (&qf)[2][Cfg<D>::kSteps], const float (&lz)[2][16],
+                                  float c, int wt, float* red_row) {
+  using C = Cfg<D>;
+  constexpr int WT = 4 / WR, SUBS = 4 / WT, UNITS = 2 * SUBS;
+  const int lane = threadIdx.x & 63;
+  Frag kf[2][C::kSteps];
+  read_kfrag<D>(buf, wt, kf[0]);
+  f32x16 acc = mfma_chain<C::kSteps>(qf[0], kf[0]);
+  float part = 0.f;
+#pragma unroll
+  for (int u = 0; u < UNITS; ++u) {
+    const int si = u >> 1, rb = u & 1;
+    f32x16 nxt = {};
+    if (u + 1 < UNITS) {
+      const int si1 = (u + 1) >> 1, rb1 = (u + 1) & 1;
+      if (rb == 0 && si + 1 < SUBS) read_kfrag<D>(buf, wt + (si + 1) * WT, kf[(si + 1) & 1]);
+      nxt = mfma_chain<C::kSteps>(qf[rb1], kf[si1 & 1]);
+    }
+    part += attn_sum(acc, c, lz[rb]);
+    interleave<C::kSteps, 6>();
+    if (rb == 1) {
+      part += __shfl_xor(part, 32);
+      red_row[(wt + si * WT) * 32 + (lane & 31)] = part;  // both half-waves hold the same sum
+      part = 0.f;
+    }
+    acc = nxt;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kGuideThreads, 2) void k_guide_attn(GuideArgs a) {
   Work w;
   if (!decode(a, w)) return;
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t kt[2][kMacroTokens * C::kStride];
+  __shared__ __attribute__((aligned(1024))) char kt[2][C::kTileBytes];
   __shared__ float red[2][4][kMacroTokens];
 
   const int lane = threadIdx.x & 63;
-  const WaveRole role = wave_role(w);
-  const int wrow0 = w.row0 + role.wr * kRowsPerWave;
-  const bool blk_ok[2] = {wrow0 < w.rows, wrow0 + 32 < w.rows};
+  const int wave = uniform(threadIdx.x >> 6);
+  const int WR = w.nrows > 128 ? 4 : (w.nrows > 64 ? 2 : 1);
+  const int wr = wave % WR, wt = wave / WR;
+  const int wrow0 = w.row0 + wr * kRowsPerWave;
 
   Frag qf[2][C::kSteps];
   load_q<D>(a, w, wrow0, qf);
@@ -287,41 +386,25 @@ __global__ __launch_bounds__(kGuideThreads, 2) void k_guide_attn(GuideArgs a) {
   const uint16_t* kseg = a.k + ((int64_t)w.seg * a.n_tot + w.n0) * D;
   float* raw_out = a.raw + ((int64_t)w.rg * a.L * a.Hkv + w.seg) * a.n_tot + w.n0;
   const int ntiles = (int)((w.c1 - w.c0 + kMacroTokens - 1) / kMacroTokens);
-  uint4 stage[C::kLoads];
-  load_tile<D>(kseg, w.c0, w.c1, stage);
-  store_tile<D>(kt[0], stage);
+  issue_tile<D>(kseg, w.c0, w.c1, kt[0], wave);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int it = 0; it < ntiles; ++it) {
     const int64_t t0 = w.c0 + (int64_t)it * kMacroTokens;
-    if (it + 1 < ntiles) load_tile<D>(kseg, t0 + kMacroTokens, w.c1, stage);
-    const uint16_t* buf = kt[it & 1];
-    for (int st = role.wt; st < kMacroTokens / 32; st += role.WT) {
-      if (t0 + st * 32 >= w.c1) break;
-      Frag kf[C::kSteps];
-      read_kfrag<D>(buf, st, kf);
-      float part = 0.f;
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        if (!blk_ok[rb]) continue;
-        f32x16 acc = {};
-#pragma unroll
-        for (int ks = 0; ks < C::kSteps; ++ks)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[rb][ks].v, kf[ks].v, acc, 0, 0, 0);
-        // acc[i] = <q_row, k_token>, row = (i/4)*8 + (lane/32)*4 + i%4, token = lane%32
-#pragma unroll
-        for (int i = 0; i < 16; ++i) part += __builtin_amdgcn_exp2f(fmaf(acc[i], a.c, -lz[rb][i]));
-      }
-      part += __shfl_xor(part, 32);
-      if (lane < 32) red[it & 1][role.wr][st * 32 + lane] = part;
-    }
-    if (it + 1 < ntiles) store_tile<D>(kt[(it + 1) & 1], stage);
+    if (it + 1 < ntiles) issue_tile<D>(kseg, t0 + kMacroTokens, w.c1, kt[(it + 1) & 1], wave);
+    const char* buf = kt[it & 1];
+    float* red_row = red[it & 1][wr];
+    if (WR == 4) attn_macro<D, 4>(buf, qf, lz, a.c, wt, red_row);
+    else if (WR == 2) attn_macro<D, 2>(buf, qf, lz, a.c, wt, red_row);
+    else attn_macro<D, 1>(buf, qf, lz, a.c, wt, red_row);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x < kMacroTokens) {
       const int64_t tok = t0 + threadIdx.x;
       if (tok < w.c1) {
         float v = red[it & 1][0][threadIdx.x];
-        for (int q = 1; q < role.WR; ++q) v += red[it & 1][q][threadIdx.x];
+        for (int q = 1; q < WR; ++q) v += red[it & 1][q][threadIdx.x];
         raw_out[tok] = v;
       }
     }
