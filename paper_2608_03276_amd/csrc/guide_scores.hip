@@ -14,11 +14,15 @@
 // guide rows on N, so each lane owns one row and 16 tokens (row statistics reduce inside
 // the lane); pass 2 swaps the operands, so each lane owns one token and 16 rows (the
 // token's sum over rows reduces inside the lane).  The same register fragments serve both
-// orientations because the A and B operand layouts of the instruction coincide.  K is
-// streamed HBM -> LDS in 128-token tiles with direct global-to-LDS loads (double-buffered,
-// XOR-swizzled); the guide queries of a wave stay in registers for its whole chunk.  Each
-// wave software-pipelines its 32x32 units: the MFMA chain of unit u+1 is interleaved with
-// the exp/add work of unit u, so the matrix core and the vector ALU run concurrently.
+// orientations because the A and B operand layouts of the instruction coincide.
+//
+// A workgroup (8 waves, one per CU) takes one chunk of 8192 tokens and one group of <= 256
+// guide rows.  The group's queries sit in LDS for the whole chunk.  Each wave streams its
+// own 32-token K sub-tiles: an asynchronous global->LDS copy into the wave's private
+// staging buffer runs while the wave computes the previous sub-tile from registers, so no
+// barrier is needed inside the main loop and the K fragments take no prefetch registers.
+// Inside a sub-tile the wave is software-pipelined: the MFMAs of one pair of 32-row blocks
+// run while the vector ALU does the softmax work of the previous pair.
 #include "tp_internal.h"
 
 namespace tp {
@@ -34,12 +38,13 @@ union Frag {
 
 template <int D>
 struct Cfg {
-  static constexpr int kSteps = D / 16;                     // MFMA k-steps over d
-  static constexpr int kPieces = D / 8;                     // 16-byte pieces per token row
+  static constexpr int kSteps = D / 16;                  // MFMA k-steps over d
+  static constexpr int kPieces = D / 8;                  // 16-byte pieces per row
   static constexpr int kRowBytes = D * 2;
-  static constexpr int kTileBytes = kMacroTokens * kRowBytes;
-  static constexpr int kRowsPerLoad = 1024 / kRowBytes;     // token rows one wave-wide 16 B load fills
-  static constexpr int kLoadsPerWave = kTileBytes / 1024 / 4;
+  static constexpr int kStride = kRowBytes + 16;         // LDS bytes per staged query row
+  static constexpr int kStageBytes = 32 * kRowBytes;     // one K sub-tile
+  static constexpr int kTokPerKB = 1024 / kRowBytes;     // tokens per 1 KB copy instruction
+  static constexpr int kSubPerWave = kChunkTokens / 32 / kGuideWaves;
 };
 
 struct Work {
@@ -83,210 +88,274 @@ __device__ inline int64_t grow_of(const GuideArgs& a, const Work& w, int rho) {
   return ((int64_t)w.l * a.Hq + qh) * a.g_tot + w.g0 + j;
 }
 
+// The row group's guide queries in LDS: local row rr at rr * kStride bytes.  The 16-byte pad
+// per row makes 16 consecutive rows start on different bank groups, so the fragment reads
+// below are conflict-free, and every fragment address is one per-lane base plus a constant.
+// Rows past the group's end repeat its last row (finite data, discarded later).
 template <int D>
-__device__ inline void load_q(const GuideArgs& a, const Work& w, int wrow0, Frag (&qf)[2][Cfg<D>::kSteps]) {
+__device__ inline void stage_q(const GuideArgs& a, const Work& w, char* qs, int nrows_pad) {
+  using C = Cfg<D>;
+  for (int t = threadIdx.x; t < nrows_pad * C::kPieces; t += kGuideThreads) {
+    const int rr = t / C::kPieces, p = t % C::kPieces;
+    const int src_row = rr < w.nrows ? rr : w.nrows - 1;
+    const uint4 v = *(const uint4*)(a.q + grow_of(a, w, w.row0 + src_row) * D + p * 8);
+    *(uint4*)(qs + rr * C::kStride + p * 16) = v;
+  }
+}
+
+// Q fragment of local row block rb: row 32 rb + lane%32, the d-columns of this half-wave.
+template <int D>
+__device__ inline void read_qfrag(const char* qs, int rb, Frag (&qf)[Cfg<D>::kSteps]) {
+  using C = Cfg<D>;
+  const int lane = threadIdx.x & 63;
+  const char* base = qs + (lane & 31) * C::kStride + (lane >> 5) * C::kRowBytes / 2 + rb * 32 * C::kStride;
+#pragma unroll
+  for (int s = 0; s < C::kSteps; ++s) qf[s].u = *(const uint4*)(base + 16 * s);
+}
+
+// K sub-tiles in a wave's LDS staging buffer: token tl (0..31) of the sub-tile at
+// tl * kRowBytes, its 16-byte piece p stored in slot p ^ swz(tl).  The swizzle puts the 16
+// (D = 128) or 8 (D = 64, two rows per 256 bytes) tokens read by one group of lanes on
+// different banks.
+template <int D>
+__device__ inline int swz(int tl) {
+  return D == 128 ? (tl & 15) : ((tl >> 1) & 7);
+}
+
+// Issue the copy of the sub-tile starting at chunk token t0 into `kbuf`: each instruction
+// moves 1 KB of consecutive K rows (coalesced); lane i fills slot i of that kilobyte, so it
+// fetches the piece that the swizzle assigns to that slot.  Tokens past the chunk's `ntok`
+// repeat its last token (finite data that pass 1 masks and pass 2 never stores).
+template <int D>
+__device__ inline void dma_subtile(const char* kchunk, int t0, int ntok, char* kbuf) {
+  using C = Cfg<D>;
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const int rho = wrow0 + rb * 32 + (lane & 31);
-    if (rho < w.rows) {
-      const uint16_t* src = a.q + grow_of(a, w, rho) * D + (lane >> 5) * (D / 2);
+  for (int j = 0; j < 32 / C::kTokPerKB; ++j) {
+    const int tl = j * C::kTokPerKB + lane / C::kPieces;
+    const int p = (lane % C::kPieces) ^ swz<D>(tl);
+    const int tok = min(t0 + tl, ntok - 1);
+    const char* src = kchunk + (uint32_t)tok * C::kRowBytes + p * 16;
+    __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(kbuf + j * 1024), 16,
+                                     0, 0);
+  }
+}
+
+// K fragment of the staged sub-tile: token lane%32, the d-columns of this half-wave.
+template <int D>
+__device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) {
+  using C = Cfg<D>;
+  const int lane = threadIdx.x & 63;
+  const int tl = lane & 31;
+  const char* row = kbuf + tl * C::kRowBytes;
 #pragma unroll
-      for (int s = 0; s < Cfg<D>::kSteps; ++s) qf[rb][s].u = *(const uint4*)(src + 8 * s);
+  for (int s = 0; s < C::kSteps; ++s) {
+    const int p = (lane >> 5) * (C::kPieces / 2) + s;
+    kf[s].u = *(const uint4*)(row + ((p ^ swz<D>(tl)) * 16));
+  }
+}
+
+// The staging buffer has landed (the wave's copies are complete).  The memory clobber keeps
+// the compiler from moving LDS reads of the buffer above the wait.
+__device__ inline void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// The fragment reads of the buffer are complete, so it may be overwritten.
+__device__ inline void wait_lds_reads() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Two independent MFMA chains: row blocks rb, rb+1 against one K sub-tile.  With INIT the
+// chains accumulate onto the values already in c0, c1; otherwise they start from zero.
+template <int KS, bool Q_IS_A, bool INIT = false>
+__device__ inline void mfma_pair(const Frag (&q0)[KS], const Frag (&q1)[KS], const Frag (&k)[KS], f32x16& c0,
+                                 f32x16& c1) {
+  if (!INIT) {
+    c0 = (f32x16){};
+    c1 = (f32x16){};
+  }
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (Q_IS_A) {
+      c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q0[s].v, k[s].v, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q1[s].v, k[s].v, c1, 0, 0, 0);
     } else {
-#pragma unroll
-      for (int s = 0; s < Cfg<D>::kSteps; ++s) qf[rb][s].u = make_uint4(0, 0, 0, 0);
+      c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k[s].v, q0[s].v, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k[s].v, q1[s].v, c1, 0, 0, 0);
     }
   }
 }
 
-// The K tile of 128 tokens sits in LDS without padding; the 16-byte piece p of token row r
-// is stored at piece p ^ (r mod kPieces), which makes the fragment reads below conflict-free.
-// Each wave fills its share with direct global->LDS loads (64 lanes x 16 B = 1 KB per
-// instruction, lane i landing at byte 16 i).  Tokens past the chunk end re-load the last
-// valid row, so every LDS byte holds finite data and no load leaves the sequence.
-template <int D>
-__device__ inline void issue_tile(const uint16_t* kseg, int64_t t0, int64_t c1, char* buf, int wave) {
-  using C = Cfg<D>;
-  const int lane = threadIdx.x & 63;
-  const char* base = (const char*)(kseg + t0 * D);  // wave-uniform
-  const int last = (int)(c1 - 1 - t0);               // last valid row of this tile
+// Instruction order of one pipeline step: NDS0 LDS reads first, then a little vector work
+// (NV0 plain, NT0 transcendental instructions) while they land, then each MFMA followed by
+// an even share of the remaining vector work of the previous pair (NV plain, NT
+// transcendental, counted separately because the scheduler classes them separately) and
+// one of the NDS LDS reads that fetch the next step's query fragments.  The matrix core,
+// the vector ALU and the LDS stay busy together, and the LDS latency is covered by a step.
+template <int NDS0, int NV0, int NT0, int NDS, int NMFMA, int NV, int NT>
+__device__ inline void step_schedule() {
+  if (NDS0 > 0) __builtin_amdgcn_sched_group_barrier(0x100, NDS0, 0);
+  if (NV0 > 0) __builtin_amdgcn_sched_group_barrier(0x002, NV0, 0);
+  if (NT0 > 0) __builtin_amdgcn_sched_group_barrier(0x400, NT0, 0);
 #pragma unroll
-  for (int j = 0; j < C::kLoadsPerWave; ++j) {
-    const int blk = wave * C::kLoadsPerWave + j;  // 1 KB block of the tile
-    int r = blk * C::kRowsPerLoad + lane / C::kPieces;
-    const int p = (lane % C::kPieces) ^ (r & (C::kPieces - 1));
-    r = r < last ? r : last;
-    __builtin_amdgcn_global_load_lds((const void*)(base + (uint32_t)(r * C::kRowBytes + p * 16)),
-                                     (__attribute__((address_space(3))) void*)(buf + blk * 1024), 16, 0, 0);
+  for (int i = 0; i < NMFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, NV, 0);
+    __builtin_amdgcn_sched_group_barrier(0x400, NT, 0);
+    if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
+  __builtin_amdgcn_sched_barrier(0);
 }
 
-// K fragment of sub-tile `st` for this lane: token st*32 + lane%32, the d-columns of its
-// half-wave (lane/32), k-step s covering columns half*D/2 + 8s .. +8.
-template <int D>
-__device__ inline void read_kfrag(const char* buf, int st, Frag (&kf)[Cfg<D>::kSteps]) {
-  using C = Cfg<D>;
-  const int lane = threadIdx.x & 63;
-  const int r = st * 32 + (lane & 31);
-  const char* row = buf + r * C::kRowBytes;
-#pragma unroll
-  for (int s = 0; s < C::kSteps; ++s) {
-    const int p = (lane >> 5) * (C::kPieces / 2) + s;
-    kf[s].u = *(const uint4*)(row + ((p ^ (r & (C::kPieces - 1))) * 16));
-  }
-}
+// Keeps the vector work of a pipeline step inside the step: without a use here the
+// compiler sinks it past the loop's branches, away from the MFMAs it should overlap.
+__device__ inline void pin(float a, float b, float c, float d) { asm volatile("" ::"v"(a), "v"(b), "v"(c), "v"(d)); }
 
-template <int KS>
-__device__ inline f32x16 mfma_chain(const Frag (&a)[KS], const Frag (&b)[KS]) {
-  f32x16 acc = {};
-#pragma unroll
-  for (int s = 0; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s].v, b[s].v, acc, 0, 0, 0);
-  return acc;
-}
+// Running (max, sum) statistics start at (-FLT_MAX, 0) rather than (-inf, 0): merging a
+// unit whose logits are all -inf (masked tokens, or the empty pipeline slot before the
+// first pair) is then an exact no-op, with no special case.
+constexpr float kNoMax = -3.402823466e38f;
 
 __device__ inline void merge_stats(float& m, float& s, float m2, float s2) {
   const float mn = fmaxf(m, m2);
-  if (mn == -INFINITY) return;
   s = s * __builtin_amdgcn_exp2f(m - mn) + s2 * __builtin_amdgcn_exp2f(m2 - mn);
   m = mn;
 }
 
-// MFMA / VALU interleave: after each MFMA of the next unit, let `n` VALU ops issue.
-template <int KS, int N>
-__device__ inline void interleave() {
-#pragma unroll
-  for (int i = 0; i < KS; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, N, 0);
-  }
+__device__ inline float max16(const f32x16& x) {
+  const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
+  const float a2 = fmaxf(fmaxf(x[6], x[7]), x[8]), a3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
+  const float a4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
+  return fmaxf(fmaxf(fmaxf(a0, a1), x[15]), fmaxf(fmaxf(a2, a3), a4));
 }
 
 // ---------------------------------------------------------------------------- pass 1
-// Online (max, sum) of the scaled logits of one unit (32 tokens x 32 rows): acc[i] is the
-// logit of token (i/4)*8 + (lane/32)*4 + i%4 and row lane%32.
-template <bool PARTIAL>
-__device__ inline void stats_update(const f32x16& acc, float c, float& m, float& s, int nvalid) {
-  const int lane = threadIdx.x & 63;
-  float x[16];
+// Online (max, sum) of one unit (32 tokens x 32 rows): acc[i] is the logit of token
+// (i/4)*8 + (lane/32)*4 + i%4 and row lane%32.  c > 0, so max(x) * c = max(x * c).
+__device__ inline void stats_update(const f32x16& acc, float c, float& m, float& s) {
+  const float mn = fmaxf(m, max16(acc) * c);
+  float e[4];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) x[i] = acc[i];
-  if (PARTIAL) {
+  for (int j = 0; j < 4; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(acc[j], c, -mn));
+#pragma unroll
+  for (int i = 4; i < 16; i += 4)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] += __builtin_amdgcn_exp2f(fmaf(acc[i + j], c, -mn));
+  s = fmaf(s, __builtin_amdgcn_exp2f(m - mn), (e[0] + e[1]) + (e[2] + e[3]));
+  m = mn;
+}
+
+// One sub-tile of pass 1, software-pipelined over the NP row-block pairs: step p issues the
+// MFMAs of pair p (query fragments qa, qb, fetched during the previous step) while the
+// vector ALU turns the pending pair (pair p-1, or the previous sub-tile's last pair when
+// p = 0) into row statistics and the LDS delivers the query fragments of the next pair.
+template <int D, int NP>
+__device__ inline void stats_steps(const char* qs, const Frag (&kf)[Cfg<D>::kSteps], Frag (&qa)[Cfg<D>::kSteps],
+                                   Frag (&qb)[Cfg<D>::kSteps], f32x16& p0, f32x16& p1, float (&sm)[2 * NP],
+                                   float (&ss)[2 * NP], float c) {
+  using C = Cfg<D>;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    f32x16 n0, n1;
+    mfma_pair<C::kSteps, false>(qa, qb, kf, n0, n1);
+    const int pn = p + 1 < NP ? p + 1 : 0;
+    read_qfrag<D>(qs, 2 * pn, qa);
+    read_qfrag<D>(qs, 2 * pn + 1, qb);
+    const int rb = p == 0 ? 2 * NP - 2 : 2 * p - 2;
+    stats_update(p0, c, sm[rb], ss[rb]);
+    stats_update(p1, c, sm[rb + 1], ss[rb + 1]);
+    pin(sm[rb], ss[rb], sm[rb + 1], ss[rb + 1]);
+    step_schedule<0, 0, 0, 2 * C::kSteps, 2 * C::kSteps, 96 / (2 * C::kSteps), 34 / (2 * C::kSteps) + 1>();
+    p0 = n0;
+    p1 = n1;
+  }
+}
+
+// The ragged last sub-tile of a chunk: tokens at or past `nvalid` get logit -inf.
+template <int D, int NP>
+__device__ inline void stats_tail(const char* qs, const Frag (&kf)[Cfg<D>::kSteps], int nvalid, float (&sm)[2 * NP],
+                                  float (&ss)[2 * NP], float c) {
+  using C = Cfg<D>;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    Frag q0[C::kSteps], q1[C::kSteps];
+    read_qfrag<D>(qs, 2 * p, q0);
+    read_qfrag<D>(qs, 2 * p + 1, q1);
+    f32x16 a0, a1;
+    mfma_pair<C::kSteps, false>(q0, q1, kf, a0, a1);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int tok = (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-      x[i] = tok < nvalid ? x[i] : -INFINITY;
+      a0[i] = tok < nvalid ? a0[i] : -INFINITY;
+      a1[i] = tok < nvalid ? a1[i] : -INFINITY;
     }
-  }
-  float t0 = fmaxf(fmaxf(x[0], x[1]), x[2]), t1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
-  float t2 = fmaxf(fmaxf(x[6], x[7]), x[8]), t3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
-  float t4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
-  const float tmax = fmaxf(fmaxf(fmaxf(t0, t1), x[15]), fmaxf(fmaxf(t2, t3), t4));
-  const float mn = fmaxf(m, tmax * c);
-  float e0 = 0.f, e1 = 0.f, e2 = 0.f, e3 = 0.f;
-#pragma unroll
-  for (int i = 0; i < 16; i += 4) {
-    e0 += __builtin_amdgcn_exp2f(fmaf(x[i + 0], c, -mn));
-    e1 += __builtin_amdgcn_exp2f(fmaf(x[i + 1], c, -mn));
-    e2 += __builtin_amdgcn_exp2f(fmaf(x[i + 2], c, -mn));
-    e3 += __builtin_amdgcn_exp2f(fmaf(x[i + 3], c, -mn));
-  }
-  const float sn = s * __builtin_amdgcn_exp2f(m - mn) + ((e0 + e1) + (e2 + e3));
-  if (PARTIAL) {  // a lane whose tokens are all masked so far keeps (-inf, 0)
-    const bool keep = mn == -INFINITY;
-    s = keep ? s : sn;
-    m = keep ? m : mn;
-  } else {
-    s = sn;
-    m = mn;
+    stats_update(a0, c, sm[2 * p], ss[2 * p]);
+    stats_update(a1, c, sm[2 * p + 1], ss[2 * p + 1]);
   }
 }
 
-template <int D, int WR, bool PARTIAL>
-__device__ inline void stats_macro(const char* buf, const Frag (&qf)[2][Cfg<D>::kSteps], float c, int wt,
-                                   int64_t t0, int64_t c1, float (&m)[2], float (&s)[2]) {
-  using C = Cfg<D>;
-  constexpr int WT = 4 / WR, SUBS = 4 / WT, UNITS = 2 * SUBS;
-  Frag kf[2][C::kSteps];
-  read_kfrag<D>(buf, wt, kf[0]);
-  f32x16 acc = mfma_chain<C::kSteps>(kf[0], qf[0]);
-#pragma unroll
-  for (int u = 0; u < UNITS; ++u) {
-    const int si = u >> 1, rb = u & 1;
-    f32x16 nxt = {};
-    if (u + 1 < UNITS) {
-      const int si1 = (u + 1) >> 1, rb1 = (u + 1) & 1;
-      if (rb == 0 && si + 1 < SUBS) read_kfrag<D>(buf, wt + (si + 1) * WT, kf[(si + 1) & 1]);
-      nxt = mfma_chain<C::kSteps>(kf[si1 & 1], qf[rb1]);
-    }
-    const int64_t sub0 = t0 + (wt + si * WT) * 32;
-    const int nvalid = c1 - sub0 >= 32 ? 32 : (c1 > sub0 ? (int)(c1 - sub0) : 0);
-    stats_update<PARTIAL>(acc, c, m[rb], s[rb], nvalid);
-    interleave<C::kSteps, 7>();
-    acc = nxt;
-  }
-}
-
-template <int D>
-__global__ __launch_bounds__(kGuideThreads, 2) void k_guide_stats(GuideArgs a) {
+template <int D, int NP>
+__global__ __launch_bounds__(kGuideThreads, 1) void k_guide_stats(GuideArgs a) {
   Work w;
   if (!decode(a, w)) return;
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char kt[2][C::kTileBytes];
-  __shared__ float2 xch[4][kRowsPerGroup];
-
+  constexpr int NB = 2 * NP;  // 32-row blocks staged (rows past the group repeat its last row)
+  __shared__ __attribute__((aligned(1024))) char qs[NB * 32 * C::kStride];
+  __shared__ __attribute__((aligned(1024))) char kst[kGuideWaves * C::kStageBytes];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
-  const int WR = w.nrows > 128 ? 4 : (w.nrows > 64 ? 2 : 1);
-  const int WT = 4 / WR;
-  const int wr = wave % WR, wt = wave / WR;
-  const int wrow0 = w.row0 + wr * kRowsPerWave;
-
-  Frag qf[2][C::kSteps];
-  load_q<D>(a, w, wrow0, qf);
-  float m[2] = {-INFINITY, -INFINITY}, s[2] = {0.f, 0.f};
-
-  const uint16_t* kseg = a.k + ((int64_t)w.seg * a.n_tot + w.n0) * D;
-  const int ntiles = (int)((w.c1 - w.c0 + kMacroTokens - 1) / kMacroTokens);
-  issue_tile<D>(kseg, w.c0, w.c1, kt[0], wave);
-  __builtin_amdgcn_s_waitcnt(0);
+  char* kbuf = kst + wave * C::kStageBytes;
+  const char* kchunk = (const char*)(a.k + ((int64_t)w.seg * a.n_tot + w.n0 + w.c0) * D);
+  const int ntok = (int)(w.c1 - w.c0);
+  const int nfull = ntok / 32;
+  int st = wave;
+  if (st < nfull) dma_subtile<D>(kchunk, 32 * st, ntok, kbuf);
+  stage_q<D>(a, w, qs, NB * 32);
   __syncthreads();
 
-  for (int it = 0; it < ntiles; ++it) {
-    const int64_t t0 = w.c0 + (int64_t)it * kMacroTokens;
-    if (it + 1 < ntiles) issue_tile<D>(kseg, t0 + kMacroTokens, w.c1, kt[(it + 1) & 1], wave);
-    const char* buf = kt[it & 1];
-    if (t0 + kMacroTokens <= w.c1) {
-      if (WR == 4) stats_macro<D, 4, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
-      else if (WR == 2) stats_macro<D, 2, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
-      else stats_macro<D, 1, false>(buf, qf, a.c, wt, t0, w.c1, m, s);
-    } else {
-      if (WR == 4) stats_macro<D, 4, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
-      else if (WR == 2) stats_macro<D, 2, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
-      else stats_macro<D, 1, true>(buf, qf, a.c, wt, t0, w.c1, m, s);
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-  }
-
-  // The two half-waves hold the same rows over different tokens.
+  float sm[NB], ss[NB];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const float mo = __shfl_xor(m[rb], 32);
-    const float so = __shfl_xor(s[rb], 32);
-    merge_stats(m[rb], s[rb], mo, so);
-    if (lane < 32) xch[wt][wr * kRowsPerWave + rb * 32 + lane] = make_float2(m[rb], s[rb]);
+  for (int i = 0; i < NB; ++i) {
+    sm[i] = kNoMax;
+    ss[i] = 0.f;
+  }
+  // full sub-tiles st = wave, wave + 8, ...
+  Frag kf[C::kSteps], qa[C::kSteps], qb[C::kSteps];
+  f32x16 p0, p1;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) p0[i] = p1[i] = -INFINITY;  // empty pipeline slot
+  read_qfrag<D>(qs, 0, qa);
+  read_qfrag<D>(qs, 1, qb);
+  for (; st < nfull; st += kGuideWaves) {
+    wait_copies();
+    read_kfrag<D>(kbuf, kf);
+    wait_lds_reads();
+    if (st + kGuideWaves < nfull) dma_subtile<D>(kchunk, 32 * (st + kGuideWaves), ntok, kbuf);
+    stats_steps<D, NP>(qs, kf, qa, qb, p0, p1, sm, ss, a.c);
+  }
+  stats_update(p0, a.c, sm[NB - 2], ss[NB - 2]);
+  stats_update(p1, a.c, sm[NB - 1], ss[NB - 1]);
+  if (ntok > 32 * nfull && wave == nfull % kGuideWaves) {
+    dma_subtile<D>(kchunk, 32 * nfull, ntok, kbuf);
+    wait_copies();
+    read_kfrag<D>(kbuf, kf);
+    stats_tail<D, NP>(qs, kf, ntok - 32 * nfull, sm, ss, a.c);
+  }
+
+  // merge the half-waves (same rows, other tokens), then the waves, through LDS (the query
+  // buffer is free now)
+  __syncthreads();
+  float2* xch = (float2*)qs;  // [wave][NB * 32]
+  static_assert(kGuideWaves * NB * 32 * sizeof(float2) <= sizeof(qs), "exchange buffer");
+#pragma unroll
+  for (int rb = 0; rb < NB; ++rb) {
+    merge_stats(sm[rb], ss[rb], __shfl_xor(sm[rb], 32), __shfl_xor(ss[rb], 32));
+    if (lane < 32) xch[wave * NB * 32 + rb * 32 + lane] = make_float2(sm[rb], ss[rb]);
   }
   __syncthreads();
-  const int t = threadIdx.x;
-  if (t < WR * kRowsPerWave) {
-    const int rho = w.row0 + t;
-    if (rho < w.rows) {
-      float mm = xch[0][t].x, ss = xch[0][t].y;
-      for (int q = 1; q < WT; ++q) merge_stats(mm, ss, xch[q][t].x, xch[q][t].y);
-      const int64_t growtot = (int64_t)a.L * a.Hq * a.g_tot;
-      a.stats[(int64_t)w.chunk * growtot + grow_of(a, w, rho)] = make_float2(mm, ss);
-    }
+  const int64_t growtot = (int64_t)a.L * a.Hq * a.g_tot;
+  for (int t = threadIdx.x; t < w.nrows; t += kGuideThreads) {
+    float mm = xch[t].x, s2 = xch[t].y;
+#pragma unroll
+    for (int q = 1; q < kGuideWaves; ++q) merge_stats(mm, s2, xch[q * NB * 32 + t].x, xch[q * NB * 32 + t].y);
+    a.stats[(int64_t)w.chunk * growtot + grow_of(a, w, w.row0 + t)] = make_float2(mm, s2);
   }
 }
 
@@ -304,7 +373,7 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
   const int64_t grow = (l * a.Hq + qh) * a.g_tot + g0 + j;
   const int64_t growtot = (int64_t)a.L * a.Hq * a.g_tot;
   const int nch = (int)((nb + kChunkTokens - 1) / kChunkTokens);
-  float m = -INFINITY, s = 0.f;
+  float m = kNoMax, s = 0.f;
   for (int c = 0; c < nch; ++c) {
     const float2 v = a.stats[(int64_t)c * growtot + grow];
     merge_stats(m, s, v.x, v.y);
@@ -313,102 +382,112 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
 }
 
 // ---------------------------------------------------------------------------- pass 2
-// Normalised weights of one unit (32 rows x 32 tokens): acc[i] is the logit of row
-// (i/4)*8 + (lane/32)*4 + i%4 and token lane%32; returns the lane's sum over its 16 rows.
-__device__ inline float attn_sum(const f32x16& acc, float c, const float (&lz)[16]) {
-  float e0 = 0.f, e1 = 0.f, e2 = 0.f, e3 = 0.f;
+// The MFMA chains of pass 2 start from -lse2/c instead of zero, so a unit's accumulator
+// holds x - lse2/c and the normalised weight is exp2(acc * c).  acc[i] belongs to row
+// (i/4)*8 + (lane/32)*4 + i%4 and token lane%32; the lane sums its 16 rows.
+__device__ inline float attn_sum(const f32x16& acc, float c) {
+  float e[4];
 #pragma unroll
-  for (int i = 0; i < 16; i += 4) {
-    e0 += __builtin_amdgcn_exp2f(fmaf(acc[i + 0], c, -lz[i + 0]));
-    e1 += __builtin_amdgcn_exp2f(fmaf(acc[i + 1], c, -lz[i + 1]));
-    e2 += __builtin_amdgcn_exp2f(fmaf(acc[i + 2], c, -lz[i + 2]));
-    e3 += __builtin_amdgcn_exp2f(fmaf(acc[i + 3], c, -lz[i + 3]));
-  }
-  return (e0 + e1) + (e2 + e3);
+  for (int j = 0; j < 4; ++j) e[j] = __builtin_amdgcn_exp2f(acc[j] * c);
+#pragma unroll
+  for (int i = 4; i < 16; i += 4)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] += __builtin_amdgcn_exp2f(acc[i + j] * c);
+  return (e[0] + e[1]) + (e[2] + e[3]);
 }
 
-template <int D, int WR>
-__device__ inline void attn_macro(const char* buf, const Frag (&qf)[2][Cfg<D>::kSteps], const float (&lz)[2][16],
-                                  float c, int wt, float* red_row) {
-  using C = Cfg<D>;
-  constexpr int WT = 4 / WR, SUBS = 4 / WT, UNITS = 2 * SUBS;
+// Accumulator start values of row block rb: -lse2/c of the lane's 16 rows.
+__device__ inline void read_lz(const float* lz_s, int rb, f32x16& acc) {
   const int lane = threadIdx.x & 63;
-  Frag kf[2][C::kSteps];
-  read_kfrag<D>(buf, wt, kf[0]);
-  f32x16 acc = mfma_chain<C::kSteps>(qf[0], kf[0]);
-  float part = 0.f;
 #pragma unroll
-  for (int u = 0; u < UNITS; ++u) {
-    const int si = u >> 1, rb = u & 1;
-    f32x16 nxt = {};
-    if (u + 1 < UNITS) {
-      const int si1 = (u + 1) >> 1, rb1 = (u + 1) & 1;
-      if (rb == 0 && si + 1 < SUBS) read_kfrag<D>(buf, wt + (si + 1) * WT, kf[(si + 1) & 1]);
-      nxt = mfma_chain<C::kSteps>(qf[rb1], kf[si1 & 1]);
-    }
-    part += attn_sum(acc, c, lz[rb]);
-    interleave<C::kSteps, 6>();
-    if (rb == 1) {
-      part += __shfl_xor(part, 32);
-      red_row[(wt + si * WT) * 32 + (lane & 31)] = part;  // both half-waves hold the same sum
+  for (int g = 0; g < 4; ++g) {
+    const float4 v = *(const float4*)(lz_s + rb * 32 + g * 8 + (lane >> 5) * 4);
+    acc[4 * g + 0] = v.x;
+    acc[4 * g + 1] = v.y;
+    acc[4 * g + 2] = v.z;
+    acc[4 * g + 3] = v.w;
+  }
+}
+
+// The sum over rows is finished for a sub-tile once its last pair has been summed: add the
+// other half-wave's rows and store the token's value.
+__device__ inline void attn_flush(float part, float* raw_out, int tok0, int ntok) {
+  const int lane = threadIdx.x & 63;
+  const float v = part + __shfl_xor(part, 32);
+  const int tok = tok0 + lane;
+  if (tok0 >= 0 && lane < 32 && tok < ntok) raw_out[tok] = v;
+}
+
+// One sub-tile of pass 2, pipelined like pass 1.  `part` carries the partial row sum of the
+// sub-tile whose pairs are in the vector stage; it is flushed (for the sub-tile starting at
+// token `prev_tok0`) when that sub-tile's last pair has been added.
+template <int D, int NP>
+__device__ inline void attn_steps(const char* qs, const float* lz_s, const Frag (&kf)[Cfg<D>::kSteps],
+                                  Frag (&qa)[Cfg<D>::kSteps], Frag (&qb)[Cfg<D>::kSteps], f32x16& p0, f32x16& p1,
+                                  float& part, int prev_tok0, float* raw_out, int ntok, float c) {
+  using C = Cfg<D>;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    f32x16 n0, n1;
+    read_lz(lz_s, 2 * p, n0);
+    read_lz(lz_s, 2 * p + 1, n1);
+    mfma_pair<C::kSteps, true, true>(qa, qb, kf, n0, n1);
+    const int pn = p + 1 < NP ? p + 1 : 0;
+    read_qfrag<D>(qs, 2 * pn, qa);
+    read_qfrag<D>(qs, 2 * pn + 1, qb);
+    part += attn_sum(p0, c) + attn_sum(p1, c);
+    pin(part, part, part, part);
+    step_schedule<8, 8, 4, 2 * C::kSteps, 2 * C::kSteps, 56 / (2 * C::kSteps), 28 / (2 * C::kSteps)>();
+    if (p == 0) {
+      attn_flush(part, raw_out, prev_tok0, ntok);
       part = 0.f;
     }
-    acc = nxt;
+    p0 = n0;
+    p1 = n1;
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(kGuideThreads, 2) void k_guide_attn(GuideArgs a) {
+template <int D, int NP>
+__global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
   Work w;
   if (!decode(a, w)) return;
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char kt[2][C::kTileBytes];
-  __shared__ float red[2][4][kMacroTokens];
-
-  const int lane = threadIdx.x & 63;
+  constexpr int NB = 2 * NP;
+  __shared__ __attribute__((aligned(1024))) char qs[NB * 32 * C::kStride];
+  __shared__ __attribute__((aligned(1024))) char kst[kGuideWaves * C::kStageBytes];
+  __shared__ __attribute__((aligned(16))) float lz_s[NB * 32];
   const int wave = uniform(threadIdx.x >> 6);
-  const int WR = w.nrows > 128 ? 4 : (w.nrows > 64 ? 2 : 1);
-  const int wr = wave % WR, wt = wave / WR;
-  const int wrow0 = w.row0 + wr * kRowsPerWave;
-
-  Frag qf[2][C::kSteps];
-  load_q<D>(a, w, wrow0, qf);
-  // lse2 of the 16 rows this lane owns in each block: row = (i/4)*8 + (lane/32)*4 + i%4.
-  float lz[2][16];
-#pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int rho = wrow0 + rb * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-      lz[rb][i] = rho < w.rows ? a.lse2[grow_of(a, w, rho)] : INFINITY;
-    }
-
-  const uint16_t* kseg = a.k + ((int64_t)w.seg * a.n_tot + w.n0) * D;
-  float* raw_out = a.raw + ((int64_t)w.rg * a.L * a.Hkv + w.seg) * a.n_tot + w.n0;
-  const int ntiles = (int)((w.c1 - w.c0 + kMacroTokens - 1) / kMacroTokens);
-  issue_tile<D>(kseg, w.c0, w.c1, kt[0], wave);
-  __builtin_amdgcn_s_waitcnt(0);
+  char* kbuf = kst + wave * C::kStageBytes;
+  const char* kchunk = (const char*)(a.k + ((int64_t)w.seg * a.n_tot + w.n0 + w.c0) * D);
+  const int ntok = (int)(w.c1 - w.c0);
+  // every sub-tile, the ragged last one included: its repeated tokens are never stored
+  const int nsub = (ntok + 31) / 32;
+  int st = wave;
+  if (st < nsub) dma_subtile<D>(kchunk, 32 * st, ntok, kbuf);
+  stage_q<D>(a, w, qs, NB * 32);
+  for (int t = threadIdx.x; t < NB * 32; t += kGuideThreads)  // padding rows: exp2(-inf) = 0
+    lz_s[t] = t < w.nrows ? -a.lse2[grow_of(a, w, w.row0 + t)] / a.c : -INFINITY;
   __syncthreads();
 
-  for (int it = 0; it < ntiles; ++it) {
-    const int64_t t0 = w.c0 + (int64_t)it * kMacroTokens;
-    if (it + 1 < ntiles) issue_tile<D>(kseg, t0 + kMacroTokens, w.c1, kt[(it + 1) & 1], wave);
-    const char* buf = kt[it & 1];
-    float* red_row = red[it & 1][wr];
-    if (WR == 4) attn_macro<D, 4>(buf, qf, lz, a.c, wt, red_row);
-    else if (WR == 2) attn_macro<D, 2>(buf, qf, lz, a.c, wt, red_row);
-    else attn_macro<D, 1>(buf, qf, lz, a.c, wt, red_row);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x < kMacroTokens) {
-      const int64_t tok = t0 + threadIdx.x;
-      if (tok < w.c1) {
-        float v = red[it & 1][0][threadIdx.x];
-        for (int q = 1; q < WR; ++q) v += red[it & 1][q][threadIdx.x];
-        raw_out[tok] = v;
-      }
-    }
+  float* raw_out = a.raw + ((int64_t)w.rg * a.L * a.Hkv + w.seg) * a.n_tot + w.n0 + w.c0;
+  Frag kf[C::kSteps], qa[C::kSteps], qb[C::kSteps];
+  f32x16 p0, p1;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) p0[i] = p1[i] = -INFINITY;  // empty pipeline slot: sums to 0
+  float part = 0.f;
+  int prev = -1;  // first chunk token of the sub-tile in the vector stage (none yet)
+  read_qfrag<D>(qs, 0, qa);
+  read_qfrag<D>(qs, 1, qb);
+  for (; st < nsub; st += kGuideWaves) {
+    wait_copies();
+    read_kfrag<D>(kbuf, kf);
+    wait_lds_reads();
+    if (st + kGuideWaves < nsub) dma_subtile<D>(kchunk, 32 * (st + kGuideWaves), ntok, kbuf);
+    attn_steps<D, NP>(qs, lz_s, kf, qa, qb, p0, p1, part, prev, raw_out, ntok, a.c);
+    prev = 32 * st;
   }
+  part += attn_sum(p0, a.c) + attn_sum(p1, a.c);
+  attn_flush(part, raw_out, prev, ntok);
 }
 
 // ---------------------------------------------------------------------------- pooling
@@ -431,8 +510,30 @@ __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
   a.s_key[(int64_t)seg * a.n_tot + n0 + i] = acc * a.pool_inv;
 }
 
+template <int D, int NP>
+hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStream_t stream) {
+  const dim3 block(kGuideThreads);
+  const dim3 grid((unsigned)(a.nrg_max * a.nchunk_pad), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
+  hipLaunchKernelGGL((k_guide_stats<D, NP>), grid, block, 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
+  hipLaunchKernelGGL(k_guide_lse, lgrid, dim3(256), 0, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_guide_attn<D, NP>), grid, block, 0, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 pgrid((unsigned)((max_nb + 255) / 256), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
+  hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// NP = row-block pairs a workgroup stages: enough for the largest row group, so short
+// guides do not pay for 256 rows.
 template <int D>
 hipError_t launch_d(const GuideArgs& a, hipStream_t stream) {
+  static_assert(Cfg<D>::kSubPerWave >= 1, "chunk too small");
   int64_t max_nb = 0, max_gb = 0;
   for (int b = 0; b < a.bt.batch; ++b) {
     const int64_t nb = a.bt.ctx_off[b + 1] - a.bt.ctx_off[b];
@@ -440,21 +541,13 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream) {
     if (nb > max_nb) max_nb = nb;
     if (gb > max_gb) max_gb = gb;
   }
-  const dim3 block(kGuideThreads);
-  const dim3 grid((unsigned)(a.nrg_max * a.nchunk_pad), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_stats<D>, grid, block, 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_lse, lgrid, dim3(256), 0, stream, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_guide_attn<D>, grid, block, 0, stream, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const dim3 pgrid((unsigned)((max_nb + 255) / 256), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
-  return hipGetLastError();
+  const int64_t rows = (int64_t)a.R * max_gb < kRowsPerGroup ? (int64_t)a.R * max_gb : kRowsPerGroup;
+  switch ((rows + 63) / 64) {
+    case 1: return launch_np<D, 1>(a, max_nb, max_gb, stream);
+    case 2: return launch_np<D, 2>(a, max_nb, max_gb, stream);
+    case 3: return launch_np<D, 3>(a, max_nb, max_gb, stream);
+    default: return launch_np<D, 4>(a, max_nb, max_gb, stream);
+  }
 }
 
 }  // namespace

@@ -17,11 +17,10 @@ struct BatchArgs {
 };
 
 // ---------------------------------------------------------------- step 1 (guide scores)
-constexpr int kGuideThreads = 256;       // 4 waves of 64
-constexpr int kRowsPerWave = 64;         // two 32-row MFMA blocks per wave
+constexpr int kGuideThreads = 512;       // 8 waves of 64, two per SIMD
+constexpr int kGuideWaves = kGuideThreads / 64;
 constexpr int kRowsPerGroup = 256;       // guide rows handled by one workgroup
-constexpr int kMacroTokens = 128;        // tokens staged in LDS per iteration
-constexpr int kChunkTokens = 2048;       // tokens of one segment per workgroup
+constexpr int kChunkTokens = 8192;       // tokens of one segment per workgroup
 
 struct GuideArgs {
   const uint16_t* q;  // bf16 [L][Hq][G_tot][d]
