@@ -19,6 +19,11 @@ sys.path.insert(0, ROOT)
 METRIC = "context tokens compressed/sec (all layers+heads); achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
 
+# The ABI calls that launch exactly one kernel (timed by events around the call) and its name.
+SINGLE_KERNEL = {"tp_quantize_v_scales": "k_quantize", "tp_combine_select_topk": "k_select",
+                 "tp_compact_kv": "k_compact"}
+KERNEL_SOURCE = {"k_quantize": "quantize.hip", "k_select": "select.hip", "k_compact": "compact.hip"}
+
 
 def algorithmic_bytes(w, kept_total_per_head):
     """Compulsory HBM bytes of each step, per kernel and in total (see the design notes)."""
@@ -38,6 +43,44 @@ def algorithmic_bytes(w, kept_total_per_head):
     }
     path = LH * (n * (2 * d + 2 * d + rb + 4) + kt * (2 * d + rb + 4 + 2 * d + rb + 4 + 4)) + q_bytes
     return per, path
+
+
+def source_sha256(kernel: str) -> str:
+    import hashlib
+
+    path = os.path.join(ROOT, "paper_2608_03276_amd", "csrc", KERNEL_SOURCE[kernel])
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary of this kernel and workload, or
+    None when there is none or the kernel source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                key, val = line[2:].split(": ", 1)
+                kv[key.strip()] = val.strip().strip("`")
+    if kv.get("source_sha256") != source_sha256(kernel):
+        return None
+    return int(kv["hbm_bytes_per_launch"])
+
+
+def copy_calibration(gib: float = 1.0, reps: int = 3):
+    """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+
+    n = int(gib * (1 << 30))
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
 def cpu_baseline(w, seconds: float):
@@ -84,6 +127,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_128k")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the path shards by "
@@ -91,6 +136,10 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     from paper_2608_03276_amd import binding as B
     from synth import workloads as W
@@ -137,10 +186,14 @@ def main():
     stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(names)}
 
     per, path_bytes = algorithmic_bytes(w, ko[-1])
-    dom = max(stage_ms, key=stage_ms.get)
+    # dominant kernel: the longest of the calls that launch one kernel each, so the events around
+    # the call time that kernel alone
+    dom = max(SINGLE_KERNEL, key=lambda n: stage_ms[n])
+    kern = SINGLE_KERNEL[dom]
     achieved = per[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    traffic = measured_traffic(kern, args.workload)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kern, "call": dom,
                 "algorithmic_bytes": per[dom], "avg_ms": round(stage_ms[dom], 4)}
     path_gbs = path_bytes / (ms * 1e-3) / 1e9
     out = {
