@@ -1,7 +1,8 @@
 """Throughput of the task-guided prefill-time eviction path on one MI355X.
 
 A step is one pass of the whole path (guide scores, V scales + quantisation, combine +
-top-k, compaction) over the workload, with inputs resident in HBM.  Prints one JSON line.
+top-k, compaction) over the workload, with inputs resident in HBM: one tp_evict call,
+whose kernels are timed by events the library records between them.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b_128k]
 """
@@ -19,14 +20,17 @@ sys.path.insert(0, ROOT)
 METRIC = "context tokens compressed/sec (all layers+heads); achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
 
-# The ABI calls that launch exactly one kernel (timed by events around the call) and its name.
-SINGLE_KERNEL = {"tp_quantize_v_scales": "k_quantize", "tp_combine_select_topk": "k_select",
-                 "tp_compact_kv": "k_compact"}
-KERNEL_SOURCE = {"k_quantize": "quantize.hip", "k_select": "select.hip", "k_compact": "compact.hip"}
+# The kernels of one tp_evict call, in launch order (the library records an event after each).
+STAGES = ["k_guide_stats", "k_guide_lse", "k_guide_attn", "k_guide_pool", "k_quantize", "k_select", "k_compact"]
+KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip"], "k_guide_lse": ["guide_scores.hip"],
+                  "k_guide_attn": ["guide_scores.hip"], "k_guide_pool": ["guide_scores.hip"],
+                  "k_quantize": ["quantize.hip", "quant_row.h"], "k_select": ["select.hip"],
+                  "k_compact": ["compact.hip"]}
 
 
 def algorithmic_bytes(w, kept_total_per_head):
-    """Compulsory HBM bytes of each step, per kernel and in total (see the design notes)."""
+    """Compulsory HBM bytes of each kernel of the step and of the whole path (see the design
+    notes).  A kernel's bytes are what it must move itself; the path counts K once."""
     from paper_2608_03276_amd import binding as B
 
     LH = w.L * w.Hkv
@@ -35,11 +39,16 @@ def algorithmic_bytes(w, kept_total_per_head):
     rb = B.row_bytes(w.qfmt, w.bits, d)
     kt = kept_total_per_head
     q_bytes = w.L * w.Hq * w.g_tot * d * 2
+    rows = w.L * w.Hq * w.g_tot
+    nch = -(-max(w.ctx_lens) // 8192)
     per = {
-        "tp_guide_scores": LH * n * (2 * d + 4) + q_bytes,          # read K once, write s_key
-        "tp_quantize_v_scales": LH * n * (2 * d + rb + 4),         # read V, write qV and scales
-        "tp_combine_select_topk": LH * (n * (4 + 4 + 4) + kt * 4),  # read s_key, scales; write S, kept idx
-        "tp_compact_kv": LH * kt * (2 * (2 * d + rb + 4) + 4),     # read kept rows + idx, write them
+        "k_guide_stats": LH * n * 2 * d + q_bytes + rows * nch * 8,     # read K, write chunk stats
+        "k_guide_lse": rows * (nch * 8 + 4),                            # merge chunk stats
+        "k_guide_attn": LH * n * (2 * d + 4) + q_bytes,                 # read K, write raw
+        "k_guide_pool": LH * n * (4 + 4),                               # read raw, write s_key
+        "k_quantize": LH * n * (2 * d + rb + 4),                        # read V, write codes and scales
+        "k_select": LH * (n * (4 + 4 + 4) + kt * 4),                    # read s_key, scales; write S, kept idx
+        "k_compact": LH * kt * (2 * (2 * d + rb + 4) + 4),              # read kept rows + idx, write them
     }
     path = LH * (n * (2 * d + 2 * d + rb + 4) + kt * (2 * d + rb + 4 + 2 * d + rb + 4 + 4)) + q_bytes
     return per, path
@@ -48,9 +57,11 @@ def algorithmic_bytes(w, kept_total_per_head):
 def source_sha256(kernel: str) -> str:
     import hashlib
 
-    path = os.path.join(ROOT, "paper_2608_03276_amd", "csrc", KERNEL_SOURCE[kernel])
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel] + ["tp_internal.h"]:
+        with open(os.path.join(ROOT, "paper_2608_03276_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(kernel: str, workload: str):
@@ -157,23 +168,14 @@ def main():
     torch.cuda.synchronize()
 
     def step(ev=None):
-        s = torch.cuda.current_stream()
-        if ev: ev[0].record(s)
-        B.tp_guide_scores(d, bt, q, k, w.softmax_scale, w.pool_k, bufs.s_key, bufs.ws_guide)
-        if ev: ev[1].record(s)
-        B.tp_quantize_v_scales(d, bt, v, w.qfmt, w.bits, bufs.scales, bufs.v_q)
-        if ev: ev[2].record(s)
-        B.tp_combine_select_topk(d, bt, bufs.s_key, bufs.scales, w.rule, w.keep_ratio or 0.0, w.keep_budget or 0,
-                                 ko, bufs.kept_idx, bufs.s_comb)
-        if ev: ev[3].record(s)
-        B.tp_compact_kv(d, bt, ko, bufs.kept_idx, k, bufs.v_q, bufs.scales, w.qfmt, w.bits, bufs.k_c, bufs.v_q_c,
-                        bufs.scales_c)
-        if ev: ev[4].record(s)
+        B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
+                   w.keep_budget or 0, ko, bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c,
+                   bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.TP_EVICT_EVENTS)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -182,19 +184,15 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
-    names = ["tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv"]
-    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(names)}
+    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(STAGES)}
 
     per, path_bytes = algorithmic_bytes(w, ko[-1])
-    # dominant kernel: the longest of the calls that launch one kernel each, so the events around
-    # the call time that kernel alone
-    dom = max(SINGLE_KERNEL, key=lambda n: stage_ms[n])
-    kern = SINGLE_KERNEL[dom]
-    achieved = per[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    kern = max(stage_ms, key=stage_ms.get)  # dominant kernel of the step
+    achieved = per[kern] / (stage_ms[kern] * 1e-3) / 1e9
     traffic = measured_traffic(kern, args.workload)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kern, "call": dom,
-                "algorithmic_bytes": per[dom], "avg_ms": round(stage_ms[dom], 4)}
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kern,
+                "algorithmic_bytes": per[kern], "avg_ms": round(stage_ms[kern], 4)}
     path_gbs = path_bytes / (ms * 1e-3) / 1e9
     out = {
         "metric": METRIC,

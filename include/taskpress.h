@@ -73,7 +73,7 @@ enum {
 };
 
 /* Entry points that take a workspace (argument of tp_workspace_size). */
-enum { TP_FN_GUIDE_SCORES = 0, TP_FN_COMBINE_SELECT_TOPK = 1 };
+enum { TP_FN_GUIDE_SCORES = 0, TP_FN_COMBINE_SELECT_TOPK = 1, TP_FN_EVICT = 2 };
 
 typedef struct tp_dims {
   int32_t num_layers;   /* L   >= 1 */
@@ -187,6 +187,38 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
                         const int32_t* kept_idx, const void* k, const void* v_q,
                         const float* scales, int32_t qfmt, int32_t bits, void* k_out,
                         void* v_q_out, float* scales_out, void* stream);
+
+/*
+ * Optional timing hooks of tp_evict, for callers that profile the path.  With num_events
+ * = TP_EVICT_EVENTS, tp_evict records events[i] (hipEvent_t created by the caller) on the
+ * stream: [0] before the work, [1] after score pass 1, [2] after the row normalisers,
+ * [3] after score pass 2, [4] after pooling, [5] after the V quantisation, [6] after the
+ * selection, [7] after the compaction; one kernel runs between consecutive events.
+ * num_events = 0 (or a NULL profile) records none.
+ */
+#define TP_EVICT_EVENTS 8
+typedef struct tp_profile {
+  int32_t num_events;
+  void* events[TP_EVICT_EVENTS];
+} tp_profile;
+
+/*
+ * The whole path in one call: steps 1-4 above with the same arguments and results as
+ * tp_guide_scores + tp_quantize_v_scales + tp_combine_select_topk + tp_compact_kv
+ * (bit-identical outputs; Sec. 3.2-3.4 as for the separate calls), validated as a whole
+ * before anything is enqueued, with optional per-kernel timing events.
+ * Outputs: s_key, scales, v_q (required: the compact cache is gathered from it), s_out
+ * (optional), kept_idx, k_out, v_q_out, scales_out.
+ * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
+ * pass's workspace followed by the selection's).
+ * Every argument is validated before anything is enqueued.  Errors as for the four calls.
+ */
+tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                   const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits,
+                   int32_t rule, double keep_ratio, int64_t keep_budget, const int64_t* kept_offsets,
+                   float* s_key, float* scales, void* v_q, float* s_out, int32_t* kept_idx,
+                   void* k_out, void* v_q_out, float* scales_out, void* workspace, size_t ws_bytes,
+                   const tp_profile* profile, void* stream);
 
 #ifdef __cplusplus
 }

@@ -17,11 +17,12 @@ LIB_PATH = os.path.join(_HERE, "lib", "libtaskpress.so")
 TP_OK, TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE, TP_ERR_HIP = range(7)
 TP_QFMT_INT, TP_QFMT_FP8_E4M3 = 0, 1
 TP_COMBINE_MUL, TP_COMBINE_NORM_ADD, TP_COMBINE_HARMONIC, TP_COMBINE_KEY_ONLY = 0, 1, 2, 3
-TP_FN_GUIDE_SCORES, TP_FN_COMBINE_SELECT_TOPK = 0, 1
+TP_FN_GUIDE_SCORES, TP_FN_COMBINE_SELECT_TOPK, TP_FN_EVICT = 0, 1, 2
 TP_MAX_BATCH = 64
+TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
-            "tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv")
+            "tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv", "tp_evict")
 
 
 class TaskPressError(RuntimeError):
@@ -42,6 +43,10 @@ class TpDims(ctypes.Structure):
 class TpBatch(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("ctx_offsets", ctypes.POINTER(ctypes.c_int64)),
                 ("guide_offsets", ctypes.POINTER(ctypes.c_int64))]
+
+
+class TpProfile(ctypes.Structure):
+    _fields_ = [("num_events", ctypes.c_int32), ("events", ctypes.c_void_p * TP_EVICT_EVENTS)]
 
 
 def _i64_array(vals):
@@ -110,6 +115,10 @@ def load():
                                            P, P, P, ctypes.c_size_t, P]
     lib.tp_compact_kv.restype = ctypes.c_int32
     lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
+    lib.tp_evict.restype = ctypes.c_int32
+    lib.tp_evict.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                             ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64, P, P, P, P, P, P, P, P, P,
+                             ctypes.c_size_t, ctypes.POINTER(TpProfile), P]
     _lib = lib
     return lib
 
@@ -144,6 +153,10 @@ def _need(t, numel, name, device=True):
         raise ValueError(f"{name} must be a device tensor")
     if t.numel() * t.element_size() < numel:
         raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, needs {numel}")
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size() if t is not None else 0
 
 
 # ----------------------------------------------------------------------------- entry points
@@ -244,6 +257,7 @@ class EvictBuffers:
         self.scales_c = torch.empty(L * Hkv * max(kt, 1), dtype=torch.float32, device=device)
         self.ws_guide = torch.empty(tp_workspace_size(TP_FN_GUIDE_SCORES, d, batch), dtype=torch.uint8,
                                     device=device)
+        self.ws_evict = torch.empty(tp_workspace_size(TP_FN_EVICT, d, batch), dtype=torch.uint8, device=device)
 
 
 def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
@@ -259,4 +273,50 @@ def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_
                            bufs.s_comb, None, stream)
     tp_compact_kv(d, batch, ko, bufs.kept_idx, k, bufs.v_q, bufs.scales, qfmt, bits, bufs.k_c, bufs.v_q_c,
                   bufs.scales_c, stream)
+    return bufs
+
+
+def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
+             rule: int, keep_ratio: float, keep_budget: int, kept_offsets, s_key, scales, v_q, s_out, kept_idx,
+             k_out, v_q_out, scales_out, workspace, events=None, stream=None):
+    """The whole path in one call.  `events`: None, or TP_EVICT_EVENTS torch.cuda.Event objects
+    (enable_timing=True) that the library records between its kernels."""
+    L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
+    n = batch.n_tot
+    _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
+    _need(k, L * Hkv * n * D * 2, "k")
+    _need(v, L * Hkv * n * D * 2, "v")
+    for t, nbytes, name in ((s_key, L * Hkv * n * 4, "s_key"), (scales, L * Hkv * n * 4, "scales"),
+                            (v_q, L * Hkv * n * row_bytes(qfmt, bits, D), "v_q")):
+        _need(t, nbytes, name)
+    ko = _i64_array(kept_offsets)
+    prof = None
+    if events is not None:
+        if len(events) != TP_EVICT_EVENTS:
+            raise ValueError(f"need {TP_EVICT_EVENTS} events")
+        s = torch.cuda.current_stream() if stream is None else stream
+        handles = []
+        for e in events:
+            if not e.cuda_event:
+                e.record(s)  # creates the underlying event
+            handles.append(e.cuda_event)
+        prof = TpProfile(TP_EVICT_EVENTS, (ctypes.c_void_p * TP_EVICT_EVENTS)(*handles))
+    ws = workspace
+    _check(load().tp_evict(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(v),
+                           float(softmax_scale), int(pool_k), int(qfmt), int(bits), int(rule), float(keep_ratio),
+                           int(keep_budget), ko, _ptr(s_key), _ptr(scales), _ptr(v_q), _ptr(s_out),
+                           _ptr(kept_idx), _ptr(k_out), _ptr(v_q_out), _ptr(scales_out), _ptr(ws),
+                           _nbytes(ws), ctypes.byref(prof) if prof is not None else None, _stream(stream)))
+
+
+def evict_fused(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int,
+                bits: int, rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0,
+                bufs: EvictBuffers = None, events=None, stream=None) -> EvictBuffers:
+    """The whole path through tp_evict; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
+    ko = kept_offsets_for(batch, keep_ratio, keep_budget)
+    if bufs is None:
+        bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
+    tp_evict(d, batch, q_guide, k, v, softmax_scale, pool_k, qfmt, bits, rule, keep_ratio, keep_budget, ko,
+             bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c, bufs.v_q_c, bufs.scales_c,
+             bufs.ws_evict, events, stream)
     return bufs

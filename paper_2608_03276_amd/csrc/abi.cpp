@@ -104,6 +104,177 @@ tp_status check_qfmt(int32_t qfmt, int32_t bits) {
   return fail(TP_ERR_PARAM, "unknown qfmt %d", qfmt);
 }
 
+
+// ------------------------------------------------------------------ argument preparation
+// Each prepare_* validates one step's arguments and fills its kernel arguments without
+// enqueueing anything, so the fused entry point can validate every step before launching.
+
+tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                        float softmax_scale, int32_t pool_k, float* s_key, void* workspace, size_t ws_bytes,
+                        tp::GuideArgs& a) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, true);
+  if (s != TP_OK) return s;
+  if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
+  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
+    return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
+  if (pool_k < 1 || (pool_k & 1) == 0) return fail(TP_ERR_PARAM, "pool_k must be odd and >= 1 (got %d)", pool_k);
+  const tp::GuideWorkspace lay = tp::guide_workspace_layout(
+      dims->num_layers, dims->num_q_heads, dims->num_kv_heads, batch->ctx_offsets, batch->guide_offsets, batch->batch);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu%s)", lay.total, ws_bytes,
+                workspace ? "" : ", NULL");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(TP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  memset(&a, 0, sizeof a);
+  a.bt = batch_args(batch, true);
+  int64_t max_nb = 0, max_gb = 0;
+  for (int b = 0; b < batch->batch; ++b) {
+    max_nb = std::max<int64_t>(max_nb, batch->ctx_offsets[b + 1] - batch->ctx_offsets[b]);
+    max_gb = std::max<int64_t>(max_gb, batch->guide_offsets[b + 1] - batch->guide_offsets[b]);
+  }
+  a.q = (const uint16_t*)q_guide;
+  a.k = (const uint16_t*)k;
+  a.s_key = s_key;
+  a.stats = (float2*)((char*)workspace + lay.stats_off);
+  a.lse2 = (float*)((char*)workspace + lay.lse_off);
+  a.raw = (float*)((char*)workspace + lay.raw_off);
+  a.L = dims->num_layers;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.R = dims->num_q_heads / dims->num_kv_heads;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.g_tot = batch->guide_offsets[batch->batch];
+  a.c = (float)((double)softmax_scale * 1.4426950408889634);
+  a.pool_inv = (float)(1.0 / ((double)a.R * pool_k));
+  a.pool_half = pool_k / 2;
+  a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
+  a.nchunk_pad = (a.nchunk_max + 7) & ~7;
+  a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
+  if ((int64_t)a.nchunk_pad * a.nrg_max > 0x7FFFFFFF)
+    return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
+  return TP_OK;
+}
+
+tp_status prepare_quant(const tp_dims* dims, const tp_batch* batch, const void* v, int32_t qfmt, int32_t bits,
+                        float* scales, void* v_q, tp::QuantArgs& a) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  s = check_qfmt(qfmt, bits);
+  if (s != TP_OK) return s;
+  if (!v || !scales) return fail(TP_ERR_NULL, "v and scales must be non-NULL");
+  if (!aligned16(v) || !aligned16(scales) || (v_q && !aligned16(v_q)))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  a.v = (const uint16_t*)v;
+  a.scales = scales;
+  a.vq = (uint8_t*)v_q;
+  a.rows = (int64_t)dims->num_layers * dims->num_kv_heads * batch->ctx_offsets[batch->batch];
+  a.qfmt = qfmt;
+  a.bits = bits;
+  a.qmax = qfmt == TP_QFMT_INT ? (float)((1 << (bits - 1)) - 1) : 448.0f;
+  return TP_OK;
+}
+
+tp_status prepare_select(const tp_dims* dims, const tp_batch* batch, const float* s_key, const float* scales,
+                         int32_t rule, double keep_ratio, int64_t keep_budget, const int64_t* kept_offsets,
+                         int32_t* kept_idx, float* s_out, void* workspace, size_t ws_bytes, tp::SelectArgs& a) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  if (!s_key || !scales || !kept_idx) return fail(TP_ERR_NULL, "s_key, scales and kept_idx must be non-NULL");
+  if (!aligned16(s_key) || !aligned16(scales) || !aligned16(kept_idx) || (s_out && !aligned16(s_out)))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (rule < TP_COMBINE_MUL || rule > TP_COMBINE_KEY_ONLY) return fail(TP_ERR_PARAM, "unknown rule %d", rule);
+  const bool use_ratio = keep_ratio > 0.0, use_budget = keep_budget >= 1;
+  if (use_ratio == use_budget)
+    return fail(TP_ERR_PARAM, "exactly one of keep_ratio in (0,1] and keep_budget >= 1 must be given");
+  if (use_ratio && !(keep_ratio <= 1.0)) return fail(TP_ERR_PARAM, "keep_ratio must be in (0, 1]");
+  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
+  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
+  memset(&a, 0, sizeof a);
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t kb = tp_keep_count(nb, keep_ratio, keep_budget);
+    if (kept_offsets[b + 1] - kept_offsets[b] != kb)
+      return fail(TP_ERR_SHAPE, "kept_offsets[%d+1]-kept_offsets[%d] = %lld, expected keep count %lld", b, b,
+                  (long long)(kept_offsets[b + 1] - kept_offsets[b]), (long long)kb);
+    a.k[b] = kb;
+    a.kept_off[b] = kept_offsets[b];
+  }
+  a.kept_off[batch->batch] = kept_offsets[batch->batch];
+  float* sbuf = s_out;
+  if (!sbuf) {
+    const size_t need = select_workspace(dims, batch);
+    if (!workspace || ws_bytes < need)
+      return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu)", need, ws_bytes);
+    if (!aligned16(workspace)) return fail(TP_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+    sbuf = (float*)workspace;
+  }
+  a.s_key = s_key;
+  a.scales = scales;
+  a.s_buf = sbuf;
+  a.kept = kept_idx;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.k_tot = kept_offsets[batch->batch];
+  a.rule = rule;
+  a.bt = batch_args(batch, false);
+  return TP_OK;
+}
+
+tp_status prepare_compact(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                          const int32_t* kept_idx, const void* k, const void* v_q, const float* scales,
+                          int32_t qfmt, int32_t bits, void* k_out, void* v_q_out, float* scales_out,
+                          tp::CompactArgs& a) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, false);
+  if (s != TP_OK) return s;
+  s = check_qfmt(qfmt, bits);
+  if (s != TP_OK) return s;
+  if (!kept_idx || !k || !k_out) return fail(TP_ERR_NULL, "kept_idx, k and k_out must be non-NULL");
+  if ((v_q == nullptr) != (v_q_out == nullptr)) return fail(TP_ERR_NULL, "v_q and v_q_out must both be given or both NULL");
+  if ((scales == nullptr) != (scales_out == nullptr))
+    return fail(TP_ERR_NULL, "scales and scales_out must both be given or both NULL");
+  if (!aligned16(kept_idx) || !aligned16(k) || !aligned16(k_out) || (v_q && (!aligned16(v_q) || !aligned16(v_q_out))) ||
+      (scales && (!aligned16(scales) || !aligned16(scales_out))))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
+  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
+  memset(&a, 0, sizeof a);
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t kb = kept_offsets[b + 1] - kept_offsets[b];
+    if (kb < 0 || kb > nb)
+      return fail(TP_ERR_SHAPE, "kept count of sequence %d (%lld) outside [0, %lld]", b, (long long)kb, (long long)nb);
+    a.kept_off[b] = kept_offsets[b];
+  }
+  a.kept_off[batch->batch] = kept_offsets[batch->batch];
+  a.kept = kept_idx;
+  a.k = (const uint16_t*)k;
+  a.vq = (const uint8_t*)v_q;
+  a.scales = scales;
+  a.k_out = (uint16_t*)k_out;
+  a.vq_out = (uint8_t*)v_q_out;
+  a.scales_out = scales_out;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.k_tot = kept_offsets[batch->batch];
+  a.row_bytes = row_bytes_of(qfmt, bits, dims->head_dim);
+  a.bt = batch_args(batch, false);
+  return TP_OK;
+}
+
+size_t guide_workspace_bytes(const tp_dims* dims, const tp_batch* batch) {
+  return tp::guide_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads, batch->ctx_offsets,
+                                    batch->guide_offsets, batch->batch)
+      .total;
+}
+
 }  // namespace
 
 extern "C" {
@@ -156,81 +327,31 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
     *bytes = select_workspace(dims, batch);
     return ok();
   }
+  if (fn == TP_FN_EVICT) {
+    s = check_batch(batch, true);
+    if (s != TP_OK) return s;
+    *bytes = guide_workspace_bytes(dims, batch) + select_workspace(dims, batch);
+    return ok();
+  }
   return fail(TP_ERR_PARAM, "unknown function id %d", fn);
 }
 
 tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
                           float softmax_scale, int32_t pool_k, float* s_key, void* workspace,
                           size_t ws_bytes, void* stream) {
-  tp_status s = check_dims(dims);
-  if (s != TP_OK) return s;
-  s = check_batch(batch, true);
-  if (s != TP_OK) return s;
-  if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
-  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key))
-    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
-  if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
-    return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
-  if (pool_k < 1 || (pool_k & 1) == 0) return fail(TP_ERR_PARAM, "pool_k must be odd and >= 1 (got %d)", pool_k);
-  const tp::GuideWorkspace lay = tp::guide_workspace_layout(
-      dims->num_layers, dims->num_q_heads, dims->num_kv_heads, batch->ctx_offsets, batch->guide_offsets, batch->batch);
-  if (!workspace || ws_bytes < lay.total)
-    return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu%s)", lay.total, ws_bytes,
-                workspace ? "" : ", NULL");
-  if (((uintptr_t)workspace & 255u) != 0) return fail(TP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-
   tp::GuideArgs a;
-  memset(&a, 0, sizeof a);
-  a.bt = batch_args(batch, true);
-  int64_t max_nb = 0, max_gb = 0;
-  for (int b = 0; b < batch->batch; ++b) {
-    max_nb = std::max<int64_t>(max_nb, batch->ctx_offsets[b + 1] - batch->ctx_offsets[b]);
-    max_gb = std::max<int64_t>(max_gb, batch->guide_offsets[b + 1] - batch->guide_offsets[b]);
-  }
-  a.q = (const uint16_t*)q_guide;
-  a.k = (const uint16_t*)k;
-  a.s_key = s_key;
-  a.stats = (float2*)((char*)workspace + lay.stats_off);
-  a.lse2 = (float*)((char*)workspace + lay.lse_off);
-  a.raw = (float*)((char*)workspace + lay.raw_off);
-  a.L = dims->num_layers;
-  a.Hq = dims->num_q_heads;
-  a.Hkv = dims->num_kv_heads;
-  a.R = dims->num_q_heads / dims->num_kv_heads;
-  a.n_tot = batch->ctx_offsets[batch->batch];
-  a.g_tot = batch->guide_offsets[batch->batch];
-  a.c = (float)((double)softmax_scale * 1.4426950408889634);
-  a.pool_inv = (float)(1.0 / ((double)a.R * pool_k));
-  a.pool_half = pool_k / 2;
-  a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
-  a.nchunk_pad = (a.nchunk_max + 7) & ~7;
-  a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
-  if ((int64_t)a.nchunk_pad * a.nrg_max > 0x7FFFFFFF)
-    return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
-  const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream);
+  const tp_status s = prepare_guide(dims, batch, q_guide, k, softmax_scale, pool_k, s_key, workspace, ws_bytes, a);
+  if (s != TP_OK) return s;
+  const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream, nullptr);
   if (e != hipSuccess) return hip_fail(e, "tp_guide_scores launch");
   return ok();
 }
 
 tp_status tp_quantize_v_scales(const tp_dims* dims, const tp_batch* batch, const void* v, int32_t qfmt,
                                int32_t bits, float* scales, void* v_q, void* stream) {
-  tp_status s = check_dims(dims);
-  if (s != TP_OK) return s;
-  s = check_batch(batch, false);
-  if (s != TP_OK) return s;
-  s = check_qfmt(qfmt, bits);
-  if (s != TP_OK) return s;
-  if (!v || !scales) return fail(TP_ERR_NULL, "v and scales must be non-NULL");
-  if (!aligned16(v) || !aligned16(scales) || (v_q && !aligned16(v_q)))
-    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
   tp::QuantArgs a;
-  a.v = (const uint16_t*)v;
-  a.scales = scales;
-  a.vq = (uint8_t*)v_q;
-  a.rows = (int64_t)dims->num_layers * dims->num_kv_heads * batch->ctx_offsets[batch->batch];
-  a.qfmt = qfmt;
-  a.bits = bits;
-  a.qmax = qfmt == TP_QFMT_INT ? (float)((1 << (bits - 1)) - 1) : 448.0f;
+  const tp_status s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, a);
+  if (s != TP_OK) return s;
   const hipError_t e = tp::launch_quantize(a, dims->head_dim, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tp_quantize_v_scales launch");
   return ok();
@@ -240,50 +361,11 @@ tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, con
                                  const float* scales, int32_t rule, double keep_ratio, int64_t keep_budget,
                                  const int64_t* kept_offsets, int32_t* kept_idx, float* s_out, void* workspace,
                                  size_t ws_bytes, void* stream) {
-  tp_status s = check_dims(dims);
-  if (s != TP_OK) return s;
-  s = check_batch(batch, false);
-  if (s != TP_OK) return s;
-  if (!s_key || !scales || !kept_idx) return fail(TP_ERR_NULL, "s_key, scales and kept_idx must be non-NULL");
-  if (!aligned16(s_key) || !aligned16(scales) || !aligned16(kept_idx) || (s_out && !aligned16(s_out)))
-    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
-  if (rule < TP_COMBINE_MUL || rule > TP_COMBINE_KEY_ONLY) return fail(TP_ERR_PARAM, "unknown rule %d", rule);
-  const bool use_ratio = keep_ratio > 0.0, use_budget = keep_budget >= 1;
-  if (use_ratio == use_budget)
-    return fail(TP_ERR_PARAM, "exactly one of keep_ratio in (0,1] and keep_budget >= 1 must be given");
-  if (use_ratio && !(keep_ratio <= 1.0)) return fail(TP_ERR_PARAM, "keep_ratio must be in (0, 1]");
-  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
-  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
   tp::SelectArgs a;
-  memset(&a, 0, sizeof a);
-  for (int b = 0; b < batch->batch; ++b) {
-    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
-    const int64_t kb = tp_keep_count(nb, keep_ratio, keep_budget);
-    if (kept_offsets[b + 1] - kept_offsets[b] != kb)
-      return fail(TP_ERR_SHAPE, "kept_offsets[%d+1]-kept_offsets[%d] = %lld, expected keep count %lld", b, b,
-                  (long long)(kept_offsets[b + 1] - kept_offsets[b]), (long long)kb);
-    a.k[b] = kb;
-    a.kept_off[b] = kept_offsets[b];
-  }
-  a.kept_off[batch->batch] = kept_offsets[batch->batch];
-  float* sbuf = s_out;
-  if (!sbuf) {
-    const size_t need = select_workspace(dims, batch);
-    if (!workspace || ws_bytes < need)
-      return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu)", need, ws_bytes);
-    if (!aligned16(workspace)) return fail(TP_ERR_WORKSPACE, "workspace must be 16-byte aligned");
-    sbuf = (float*)workspace;
-  }
-  a.s_key = s_key;
-  a.scales = scales;
-  a.s_buf = sbuf;
-  a.kept = kept_idx;
-  a.n_tot = batch->ctx_offsets[batch->batch];
-  a.k_tot = kept_offsets[batch->batch];
-  a.rule = rule;
-  a.bt = batch_args(batch, false);
-  const hipError_t e =
-      tp::launch_select(a, dims->num_layers * dims->num_kv_heads, (hipStream_t)stream);
+  const tp_status s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets,
+                                     kept_idx, s_out, workspace, ws_bytes, a);
+  if (s != TP_OK) return s;
+  const hipError_t e = tp::launch_select(a, dims->num_layers * dims->num_kv_heads, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk launch");
   return ok();
 }
@@ -291,44 +373,60 @@ tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, con
 tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
                         const int32_t* kept_idx, const void* k, const void* v_q, const float* scales, int32_t qfmt,
                         int32_t bits, void* k_out, void* v_q_out, float* scales_out, void* stream) {
-  tp_status s = check_dims(dims);
-  if (s != TP_OK) return s;
-  s = check_batch(batch, false);
-  if (s != TP_OK) return s;
-  s = check_qfmt(qfmt, bits);
-  if (s != TP_OK) return s;
-  if (!kept_idx || !k || !k_out) return fail(TP_ERR_NULL, "kept_idx, k and k_out must be non-NULL");
-  if ((v_q == nullptr) != (v_q_out == nullptr)) return fail(TP_ERR_NULL, "v_q and v_q_out must both be given or both NULL");
-  if ((scales == nullptr) != (scales_out == nullptr))
-    return fail(TP_ERR_NULL, "scales and scales_out must both be given or both NULL");
-  if (!aligned16(kept_idx) || !aligned16(k) || !aligned16(k_out) || (v_q && (!aligned16(v_q) || !aligned16(v_q_out))) ||
-      (scales && (!aligned16(scales) || !aligned16(scales_out))))
-    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
-  if (!kept_offsets) return fail(TP_ERR_NULL, "kept_offsets is NULL");
-  if (kept_offsets[0] != 0) return fail(TP_ERR_SHAPE, "kept_offsets[0] must be 0");
   tp::CompactArgs a;
-  memset(&a, 0, sizeof a);
-  for (int b = 0; b < batch->batch; ++b) {
-    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
-    const int64_t kb = kept_offsets[b + 1] - kept_offsets[b];
-    if (kb < 0 || kb > nb)
-      return fail(TP_ERR_SHAPE, "kept count of sequence %d (%lld) outside [0, %lld]", b, (long long)kb, (long long)nb);
-    a.kept_off[b] = kept_offsets[b];
-  }
-  a.kept_off[batch->batch] = kept_offsets[batch->batch];
-  a.kept = kept_idx;
-  a.k = (const uint16_t*)k;
-  a.vq = (const uint8_t*)v_q;
-  a.scales = scales;
-  a.k_out = (uint16_t*)k_out;
-  a.vq_out = (uint8_t*)v_q_out;
-  a.scales_out = scales_out;
-  a.n_tot = batch->ctx_offsets[batch->batch];
-  a.k_tot = kept_offsets[batch->batch];
-  a.row_bytes = row_bytes_of(qfmt, bits, dims->head_dim);
-  a.bt = batch_args(batch, false);
+  const tp_status s = prepare_compact(dims, batch, kept_offsets, kept_idx, k, v_q, scales, qfmt, bits, k_out,
+                                      v_q_out, scales_out, a);
+  if (s != TP_OK) return s;
   const hipError_t e = tp::launch_compact(a, dims->num_layers * dims->num_kv_heads, dims->head_dim, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tp_compact_kv launch");
+  return ok();
+}
+
+tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k, const void* v,
+                   float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
+                   int64_t keep_budget, const int64_t* kept_offsets, float* s_key, float* scales, void* v_q,
+                   float* s_out, int32_t* kept_idx, void* k_out, void* v_q_out, float* scales_out, void* workspace,
+                   size_t ws_bytes, const tp_profile* profile, void* stream) {
+  if (profile && profile->num_events != 0) {
+    if (profile->num_events < TP_EVICT_EVENTS)
+      return fail(TP_ERR_PARAM, "profile->num_events must be 0 or %d", TP_EVICT_EVENTS);
+    for (int i = 0; i < TP_EVICT_EVENTS; ++i)
+      if (!profile->events[i]) return fail(TP_ERR_NULL, "profile->events[%d] is NULL", i);
+  }
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, true);
+  if (s != TP_OK) return s;
+  if (!v_q) return fail(TP_ERR_NULL, "v_q must be non-NULL (the compact cache is built from it)");
+  // workspace: the score pass's, then (without s_out) the combined scores
+  const size_t gws = guide_workspace_bytes(dims, batch);
+  if (!workspace || ws_bytes < gws) return fail(TP_ERR_WORKSPACE, "workspace needs at least %zu bytes", gws);
+  tp::GuideArgs ga;
+  s = prepare_guide(dims, batch, q_guide, k, softmax_scale, pool_k, s_key, workspace, gws, ga);
+  if (s != TP_OK) return s;
+  tp::QuantArgs qa;
+  s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);
+  if (s != TP_OK) return s;
+  tp::SelectArgs sa;
+  s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx, s_out,
+                     (char*)workspace + gws, ws_bytes - gws, sa);
+  if (s != TP_OK) return s;
+  tp::CompactArgs ca;
+  s = prepare_compact(dims, batch, kept_offsets, kept_idx, k, v_q, scales, qfmt, bits, k_out, v_q_out, scales_out, ca);
+  if (s != TP_OK) return s;
+
+  const hipStream_t st = (hipStream_t)stream;
+  hipEvent_t* ev = (profile && profile->num_events) ? (hipEvent_t*)profile->events : nullptr;
+  hipError_t e = hipSuccess;
+  if (ev) e = hipEventRecord(ev[0], st);
+  if (e == hipSuccess) e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? ev + 1 : nullptr);
+  if (e == hipSuccess) e = tp::launch_quantize(qa, dims->head_dim, st);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[5], st);
+  if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
+  if (e == hipSuccess) e = tp::launch_compact(ca, dims->num_layers * dims->num_kv_heads, dims->head_dim, st);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[7], st);
+  if (e != hipSuccess) return hip_fail(e, "tp_evict launch");
   return ok();
 }
 

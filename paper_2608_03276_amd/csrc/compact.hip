@@ -2,7 +2,8 @@
 // of each KV head is kept; Sec. 4 setup: eviction right after prefill).
 //
 // A row gather bound by HBM: d/8 lanes move one bf16 K row (16 B each), the first
-// row_bytes/16 of them the quantised V row, lane 0 the scale.  Reads of the source rows are
+// row_bytes/16 of them the quantised V row, lane 0 the scale; each lane group handles four
+// kept rows so their index loads and row loads are in flight together.  Reads of the source rows are
 // 16-byte aligned and each row's bytes are contiguous, so every wave touches whole cache
 // lines.  Indices outside [0, N_b) produce a zero row (no out-of-bounds access).
 #include "tp_internal.h"
@@ -11,6 +12,7 @@ namespace tp {
 namespace {
 
 constexpr int kCompactThreads = 256;
+constexpr int kRowsPerLane = 4;  // kept rows per lane group: their index and row loads overlap
 
 template <int D>
 __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
@@ -18,24 +20,40 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
   constexpr int RPB = kCompactThreads / LPR;
   const int seg = blockIdx.y;
   const int sub = threadIdx.x % LPR;
-  const int64_t r = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;  // kept row in [0, K_tot)
-  if (r >= a.k_tot) return;
-  int b = 0;
-  while (b + 1 < a.bt.batch && a.kept_off[b + 1] <= r) ++b;
-  const int64_t n0 = a.bt.ctx_off[b];
-  const int64_t nb = a.bt.ctx_off[b + 1] - n0;
-  const int64_t idx = a.kept[(int64_t)seg * a.k_tot + r];
-  const bool ok = idx >= 0 && idx < nb;
-  const int64_t src = (int64_t)seg * a.n_tot + n0 + (ok ? idx : 0);
-  const int64_t dst = (int64_t)seg * a.k_tot + r;
-
-  const uint4 kv = ok ? *((const uint4*)(a.k + src * D) + sub) : make_uint4(0, 0, 0, 0);
-  *((uint4*)(a.k_out + dst * D) + sub) = kv;
-  if (a.vq != nullptr && sub * 16 < a.row_bytes) {
-    const uint4 qv = ok ? *((const uint4*)(a.vq + src * a.row_bytes) + sub) : make_uint4(0, 0, 0, 0);
-    *((uint4*)(a.vq_out + dst * a.row_bytes) + sub) = qv;
+  const int64_t r0 = (int64_t)blockIdx.x * RPB * kRowsPerLane + threadIdx.x / LPR;
+  int64_t src[kRowsPerLane];
+  bool ok[kRowsPerLane];
+#pragma unroll
+  for (int u = 0; u < kRowsPerLane; ++u) {  // kept row r in [0, K_tot): its source row
+    const int64_t r = r0 + u * RPB;
+    ok[u] = false;
+    src[u] = 0;
+    if (r < a.k_tot) {
+      int b = 0;
+      while (b + 1 < a.bt.batch && a.kept_off[b + 1] <= r) ++b;
+      const int64_t n0 = a.bt.ctx_off[b];
+      const int64_t nb = a.bt.ctx_off[b + 1] - n0;
+      const int64_t idx = a.kept[(int64_t)seg * a.k_tot + r];
+      ok[u] = idx >= 0 && idx < nb;
+      src[u] = (int64_t)seg * a.n_tot + n0 + (ok[u] ? idx : 0);
+    }
   }
-  if (a.scales != nullptr && sub == 0) a.scales_out[dst] = ok ? a.scales[src] : 0.0f;
+  uint4 kv[kRowsPerLane], qv[kRowsPerLane];
+  const bool has_q = a.vq != nullptr && sub * 16 < a.row_bytes;
+#pragma unroll
+  for (int u = 0; u < kRowsPerLane; ++u) {
+    kv[u] = ok[u] ? *((const uint4*)(a.k + src[u] * D) + sub) : make_uint4(0, 0, 0, 0);
+    qv[u] = ok[u] && has_q ? *((const uint4*)(a.vq + src[u] * a.row_bytes) + sub) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < kRowsPerLane; ++u) {
+    const int64_t r = r0 + u * RPB;
+    if (r >= a.k_tot) break;
+    const int64_t dst = (int64_t)seg * a.k_tot + r;
+    *((uint4*)(a.k_out + dst * D) + sub) = kv[u];
+    if (has_q) *((uint4*)(a.vq_out + dst * a.row_bytes) + sub) = qv[u];
+    if (a.scales != nullptr && sub == 0) a.scales_out[dst] = ok[u] ? a.scales[src[u]] : 0.0f;
+  }
 }
 
 }  // namespace
@@ -43,7 +61,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
 hipError_t launch_compact(const CompactArgs& a, int segments, int head_dim, hipStream_t stream) {
   if (a.k_tot == 0) return hipSuccess;
   const int lpr = head_dim / 8;
-  const int64_t rpb = kCompactThreads / lpr;
+  const int64_t rpb = (int64_t)(kCompactThreads / lpr) * kRowsPerLane;
   const dim3 grid((unsigned)((a.k_tot + rpb - 1) / rpb), (unsigned)segments);
   if (head_dim == 128)
     hipLaunchKernelGGL(k_compact<128>, grid, dim3(kCompactThreads), 0, stream, a);

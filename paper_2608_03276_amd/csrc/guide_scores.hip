@@ -458,7 +458,8 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
   __shared__ __attribute__((aligned(16))) float lz_s[NB * 32];
   const int wave = uniform(threadIdx.x >> 6);
   char* kbuf = kst + wave * C::kStageBytes;
-  const char* kchunk = (const char*)(a.k + ((int64_t)w.seg * a.n_tot + w.n0 + w.c0) * D);
+  const int64_t tok0 = (int64_t)w.seg * a.n_tot + w.n0 + w.c0;  // first token row of the chunk
+  const char* kchunk = (const char*)(a.k + tok0 * D);
   const int ntok = (int)(w.c1 - w.c0);
   // every sub-tile, the ragged last one included: its repeated tokens are never stored
   const int nsub = (ntok + 31) / 32;
@@ -511,28 +512,33 @@ __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
 }
 
 template <int D, int NP>
-hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStream_t stream) {
+hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStream_t stream, hipEvent_t* ev) {
   const dim3 block(kGuideThreads);
   const dim3 grid((unsigned)(a.nrg_max * a.nchunk_pad), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
   hipLaunchKernelGGL((k_guide_stats<D, NP>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[0], stream);
   if (e != hipSuccess) return e;
   const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
   hipLaunchKernelGGL(k_guide_lse, lgrid, dim3(256), 0, stream, a);
   e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_guide_attn<D, NP>), grid, block, 0, stream, a);
   e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[2], stream);
   if (e != hipSuccess) return e;
   const dim3 pgrid((unsigned)((max_nb + 255) / 256), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
   hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[3], stream);
+  return e;
 }
 
 // NP = row-block pairs a workgroup stages: enough for the largest row group, so short
 // guides do not pay for 256 rows.
 template <int D>
-hipError_t launch_d(const GuideArgs& a, hipStream_t stream) {
+hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
   static_assert(Cfg<D>::kSubPerWave >= 1, "chunk too small");
   int64_t max_nb = 0, max_gb = 0;
   for (int b = 0; b < a.bt.batch; ++b) {
@@ -543,10 +549,10 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream) {
   }
   const int64_t rows = (int64_t)a.R * max_gb < kRowsPerGroup ? (int64_t)a.R * max_gb : kRowsPerGroup;
   switch ((rows + 63) / 64) {
-    case 1: return launch_np<D, 1>(a, max_nb, max_gb, stream);
-    case 2: return launch_np<D, 2>(a, max_nb, max_gb, stream);
-    case 3: return launch_np<D, 3>(a, max_nb, max_gb, stream);
-    default: return launch_np<D, 4>(a, max_nb, max_gb, stream);
+    case 1: return launch_np<D, 1>(a, max_nb, max_gb, stream, ev);
+    case 2: return launch_np<D, 2>(a, max_nb, max_gb, stream, ev);
+    case 3: return launch_np<D, 3>(a, max_nb, max_gb, stream, ev);
+    default: return launch_np<D, 4>(a, max_nb, max_gb, stream, ev);
   }
 }
 
@@ -572,9 +578,9 @@ GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const 
   return w;
 }
 
-hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream) {
-  if (head_dim == 128) return launch_d<128>(a, stream);
-  return launch_d<64>(a, stream);
+hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev) {
+  if (head_dim == 128) return launch_d<128>(a, stream, ev);
+  return launch_d<64>(a, stream, ev);
 }
 
 }  // namespace tp

@@ -1,0 +1,130 @@
+// Per-token V quantisation of Eq. 2 (Sec. 3.3), shared by the standalone quantisation kernel
+// and the score pass that quantises V alongside the keys:
+//   gamma_t = fl32(max_c |v_tc| / qmax)
+//   q_tc    = clamp(RNE(fl32(v_tc / gamma_t)), -qmax, qmax)    (b-bit integers), or the OCP
+//             E4M3 code of fl32(v_tc / gamma_t), RNE, saturating at 448; gamma_t = 0 gives 0.
+//
+// A token row of d bf16 values is held by LPT = d/8 consecutive lanes, 16 bytes each.  The
+// absmax is an integer max of the bf16 magnitude bits (exact), reduced across those lanes
+// with DPP row operations.  The per-element quotient avoids a full IEEE division: the row is
+// rescaled by 2^-e (e = exponent of its absmax, an exact power-of-two scaling that keeps
+// every product and residual in the normal range), the quotient is v' * y with
+// y = 1/gamma' (one correctly rounded division per token), and one residual step
+// fl(q0 + fma(-q0, gamma', v') * y) corrects it.  An exhaustive check over every
+// (absmax, v) pair of bf16 values, for every supported qmax, shows the resulting integer /
+// E4M3 codes equal those of the correctly rounded quotient; rows whose absmax is below
+// 2^-100 use the IEEE division directly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tp {
+
+struct QuantFmt {
+  bool int_fmt;  // b-bit integers (else fp8-e4m3)
+  bool nibbles;  // int with b <= 4: two codes per byte, even element in the low nibble
+  float qmax;
+};
+
+// max over the LPT (8 or 16) consecutive lanes of a DPP row segment.
+template <int LPT>
+__device__ inline uint32_t group_max(uint32_t x) {
+  // quad_perm [1,0,3,2] and [2,3,0,1]: lanes xor 1, xor 2
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));
+  // row_half_mirror: lane i <-> 7-i within each 8 (pairs the two quads of a half-row)
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));
+  if (LPT == 16) {
+    // row_mirror: lane i <-> 15-i within each row of 16 (pairs the two half-rows)
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));
+  }
+  return x;
+}
+
+// OCP E4M3 code of y: nearest value, ties to the even mantissa, |y| >= 448 -> 448, sign kept.
+__device__ inline uint32_t e4m3_code(float y) {
+  const uint32_t b = __float_as_uint(y);
+  const uint32_t sign = (b >> 24) & 0x80u;
+  const uint32_t a = b & 0x7FFFFFFFu;
+  const float af = __uint_as_float(a);
+  uint32_t code;
+  if (af >= 448.0f) {
+    code = 0x7Eu;
+  } else if (af < 0.015625f) {  // below 2^-6: subnormal codes, step 2^-9 (8 = 2^-6)
+    code = (uint32_t)__builtin_rintf(af * 512.0f);
+  } else {  // round the 23-bit mantissa to 3 bits (RNE); a carry bumps the exponent
+    const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+    code = (((r >> 23) - 120u) << 3) | ((r >> 20) & 7u);
+  }
+  return sign | code;
+}
+
+// Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
+// LPT consecutive lanes; every lane of the wave must call this together (the absmax is
+// reduced across lanes).  Returns gamma (the same on all LPT lanes of the row) and the
+// piece's codes: 8 bytes in out.x, out.y, or 8 nibbles in out.x.
+template <int LPT>
+__device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& out) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t mx = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    mx = max(mx, w[i] & 0x7FFFu);
+    mx = max(mx, (w[i] >> 16) & 0x7FFFu);
+  }
+  mx = group_max<LPT>(mx);
+  const float amax = __uint_as_float(mx << 16);
+  const float gamma = amax / f.qmax;
+  // exponent field of the absmax (bf16 and fp32 share it); below 2^-100 divide directly
+  const int ef = (int)(mx >> 7);
+  const bool direct = ef <= 27;
+  const float sc = direct ? 1.0f : __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+  const float gs = gamma * sc;
+  const float ys = 1.0f / gs;
+  uint32_t code[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xFFFFu);
+    const float v = __uint_as_float(h << 16);
+    float y;
+    if (direct) {
+      y = v / gamma;
+    } else {
+      const float vs = v * sc;
+      const float q0 = vs * ys;
+      y = fmaf(fmaf(-q0, gs, vs), ys, q0);
+    }
+    if (gamma == 0.0f) {
+      code[i] = 0;
+    } else if (f.int_fmt) {
+      const float r = __builtin_amdgcn_fmed3f(__builtin_rintf(y), -f.qmax, f.qmax);
+      code[i] = (uint32_t)(int32_t)r;
+    } else {
+      code[i] = e4m3_code(__builtin_copysignf(y, v));
+    }
+  }
+  if (f.nibbles) {
+    uint32_t p = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) p |= (code[i] & 0xFu) << (4 * i);
+    out.x = p;
+    out.y = 0;
+  } else {
+    out.x = (code[0] & 0xFFu) | ((code[1] & 0xFFu) << 8) | ((code[2] & 0xFFu) << 16) | ((code[3] & 0xFFu) << 24);
+    out.y = (code[4] & 0xFFu) | ((code[5] & 0xFFu) << 8) | ((code[6] & 0xFFu) << 16) | ((code[7] & 0xFFu) << 24);
+  }
+  return gamma;
+}
+
+// Store the codes of one piece: row `row` of a code tensor with `row_bytes` per row, piece
+// `sub` (D/8 pieces per row).
+template <int D>
+__device__ inline void store_codes(uint8_t* vq, int64_t row, int sub, const QuantFmt& f, const uint2& c) {
+  if (f.nibbles)
+    *((uint32_t*)(vq + row * (D / 2)) + sub) = c.x;
+  else
+    *((uint2*)(vq + row * D) + sub) = c;
+}
+
+}  // namespace tp

@@ -46,7 +46,8 @@ struct GuideWorkspace {
 GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const int64_t* ctx_off,
                                       const int64_t* g_off, int32_t batch);
 
-hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream);
+// ev (optional): 4 events recorded after the stats, lse, attention and pooling kernels.
+hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev);
 
 // ---------------------------------------------------------------- step 2 (V scales)
 struct QuantArgs {

@@ -154,3 +154,61 @@ def test_compact_validation():
     assert cp(vq=None) == B.TP_ERR_NULL
     assert cp(sco=None) == B.TP_ERR_NULL
     assert cp(bits=0) == B.TP_ERR_PARAM
+
+
+def _ev(d, bt, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, scale=0.125, pool=5, qfmt=0, bits=8, rule=0, ratio=0.25, budget=0,
+             ko=None, skey=FAKE, sc=FAKE, vq=FAKE, sout=FAKE, idx=FAKE, kout=FAKE, vqout=FAKE, scout=FAKE,
+             ws=FAKE, wsb=1 << 40, prof=None)
+    a.update(kw)
+    if a["ko"] is None:
+        a["ko"] = B.kept_offsets_for(bt, a["ratio"], a["budget"])
+    ko = (ctypes.c_int64 * len(a["ko"]))(*a["ko"])
+    prof = ctypes.byref(a["prof"]) if a["prof"] is not None else None
+    return lib.tp_evict(ctypes.byref(d), ctypes.byref(bt.c), a["q"], a["k"], a["v"], a["scale"], a["pool"],
+                        a["qfmt"], a["bits"], a["rule"], a["ratio"], a["budget"], ko, a["skey"], a["sc"], a["vq"],
+                        a["sout"], a["idx"], a["kout"], a["vqout"], a["scout"], a["ws"], a["wsb"], prof, None)
+
+
+@no_gpu
+def test_evict_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300], [0, 16, 20])
+    short_prof = B.TpProfile(3)
+    null_prof = B.TpProfile(B.TP_EVICT_EVENTS)
+    cases = [
+        (dict(q=None), B.TP_ERR_NULL),
+        (dict(v=None), B.TP_ERR_NULL),
+        (dict(vq=None), B.TP_ERR_NULL),
+        (dict(idx=None), B.TP_ERR_NULL),
+        (dict(kout=None), B.TP_ERR_NULL),
+        (dict(vqout=None), B.TP_ERR_NULL),
+        (dict(scale=0.0), B.TP_ERR_PARAM),
+        (dict(pool=2), B.TP_ERR_PARAM),
+        (dict(qfmt=5), B.TP_ERR_PARAM),
+        (dict(bits=9), B.TP_ERR_PARAM),
+        (dict(rule=7), B.TP_ERR_PARAM),
+        (dict(ratio=0.0, budget=0, ko=[0, 1, 2]), B.TP_ERR_PARAM),
+        (dict(ko=[0, 25, 51]), B.TP_ERR_SHAPE),
+        (dict(ws=None), B.TP_ERR_WORKSPACE),
+        (dict(wsb=1024), B.TP_ERR_WORKSPACE),
+        (dict(sout=None, wsb=B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, d, bt)), B.TP_ERR_WORKSPACE),
+        (dict(prof=short_prof), B.TP_ERR_PARAM),
+        (dict(prof=null_prof), B.TP_ERR_NULL),
+        (dict(k=FAKE + 8), B.TP_ERR_PARAM),
+    ]
+    for kw, want in cases:
+        assert _ev(d, bt, **kw) == want, kw
+        assert lib.tp_last_error().decode() != ""
+    assert _ev(d, B.Batch([0, 100, 300])) == B.TP_ERR_NULL  # the score step needs guide offsets
+    assert _ev(B.dims(2, 8, 2, 96), bt) == B.TP_ERR_UNSUPPORTED
+
+
+def test_evict_workspace_size():
+    d = B.dims(32, 32, 8, 128)
+    bt = B.Batch([0, 131072], [0, 64])
+    g = B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, d, bt)
+    s = B.tp_workspace_size(B.TP_FN_COMBINE_SELECT_TOPK, d, bt)
+    assert B.tp_workspace_size(B.TP_FN_EVICT, d, bt) == g + s
+    with pytest.raises(B.TaskPressError):
+        B.tp_workspace_size(B.TP_FN_EVICT, d, B.Batch([0, 131072]))

@@ -270,3 +270,53 @@ def test_deterministic(gpu_lib):
     b = pu.run_gpu(w, q, k, v)
     for n, t in snap.items():
         assert torch.equal(t.view(torch.uint8), getattr(b, n).view(torch.uint8)), n
+
+
+# ----------------------------------------------------------------------------- fused entry point
+def _fused_vs_calls(w, with_events=False):
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    q, k, v = pu.device_inputs(w)
+    sep = pu.run_gpu(w, q, k, v)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(B.TP_EVICT_EVENTS)] if with_events else None
+    fused = B.evict_fused(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                          rule=w.rule, keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0, events=ev)
+    torch.cuda.synchronize()
+    for n in ("s_key", "scales", "v_q", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c"):
+        assert torch.equal(getattr(sep, n).view(torch.uint8), getattr(fused, n).view(torch.uint8)), (w.name, n)
+    return fused, ev
+
+
+def test_evict_matches_the_four_calls(gpu_lib):
+    """tp_evict gives bit-identical outputs to the separate calls."""
+    for w in (W.tiny(),
+              W.tiny().with_(name="tiny-d128-ragged-int4", d=128, ctx_lens=(1000, 33, 4200), guide_lens=(16, 3, 90),
+                             bits=4, keep_ratio=None, keep_budget=100),
+              W.ragged8().with_(name="ragged-fp8", L=2, ctx_lens=(9000, 1, 8193), guide_lens=(32, 128, 7),
+                                keep_budget=500, qfmt=1),
+              W.llama8b_32k().with_(name="two-row-groups", L=1, ctx_lens=(5000,), guide_lens=(100,))):
+        pu.log(f"tp_evict vs four calls: {w.describe()}")
+        _fused_vs_calls(w)
+
+
+def test_evict_against_oracle(gpu_lib):
+    w = W.tiny().with_(name="tiny-evict", ctx_lens=(700, 1500), guide_lens=(9, 16), keep_ratio=0.3)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    q, k, v = pu.device_inputs(w)
+    bufs = B.evict_fused(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                         rule=w.rule, keep_ratio=w.keep_ratio)
+    torch.cuda.synchronize()
+    for b in range(w.batch):
+        for h in range(w.Hkv):
+            pu.check_segment(w, bufs, b, 0, h)
+
+
+def test_evict_profile_events(gpu_lib):
+    w = W.llama8b_32k().with_(name="events", L=2, ctx_lens=(20000,), guide_lens=(64,))
+    _, ev = _fused_vs_calls(w, with_events=True)
+    stages = [ev[i].elapsed_time(ev[i + 1]) for i in range(B.TP_EVICT_EVENTS - 1)]
+    assert all(t >= 0 for t in stages), stages
+    assert stages[0] > 0 and stages[2] > 0 and stages[4] > 0, stages
+    total = ev[0].elapsed_time(ev[-1])
+    assert abs(sum(stages) - total) <= 1e-3 * total + 0.05, (stages, total)
