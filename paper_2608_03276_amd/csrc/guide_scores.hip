@@ -492,23 +492,56 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
 }
 
 // ---------------------------------------------------------------------------- pooling
+// s_key = (1/(R K)) * sum over the window of the raw sums of all row groups (zero outside the
+// sequence).  A block stages kPoolTile + 2*half raw values (summed over row groups) in LDS
+// with coalesced loads, then each thread sums its windows from LDS; windows wider than
+// kPoolMaxHalf use the direct loop.
+constexpr int kPoolTile = 1024;
+constexpr int kPoolMaxHalf = 512;
+
+__device__ inline float raw_at(const GuideArgs& a, const float* raw, int nrg, int64_t j) {
+  const int64_t lh = (int64_t)a.L * a.Hkv;
+  float v = 0.f;
+  for (int rg = 0; rg < nrg; ++rg) v += raw[rg * lh * a.n_tot + j];
+  return v;
+}
+
 __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
+  __shared__ float buf[kPoolTile + 2 * kPoolMaxHalf];
   const int seg = blockIdx.y, b = blockIdx.z;
   const int64_t n0 = a.bt.ctx_off[b];
   const int64_t nb = a.bt.ctx_off[b + 1] - n0;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= nb) return;
+  const int64_t i0 = (int64_t)blockIdx.x * kPoolTile;
+  if (i0 >= nb) return;
   const int gb = (int)(a.bt.g_off[b + 1] - a.bt.g_off[b]);
   const int nrg = (a.R * gb + kRowsPerGroup - 1) / kRowsPerGroup;
-  const int64_t lh = (int64_t)a.L * a.Hkv;
   const float* raw = a.raw + (int64_t)seg * a.n_tot + n0;
-  float acc = 0.f;
-  for (int t = -a.pool_half; t <= a.pool_half; ++t) {
-    const int64_t j = i + t;
-    if (j < 0 || j >= nb) continue;
-    for (int rg = 0; rg < nrg; ++rg) acc += raw[rg * lh * a.n_tot + j];
+  float* out = a.s_key + (int64_t)seg * a.n_tot + n0;
+  const int half = a.pool_half;
+  if (half > kPoolMaxHalf) {  // wide windows: direct sums
+    for (int u = 0; u < kPoolTile / 256; ++u) {
+      const int64_t i = i0 + threadIdx.x + 256 * u;
+      if (i >= nb) break;
+      float acc = 0.f;
+      for (int t = -half; t <= half; ++t)
+        if (i + t >= 0 && i + t < nb) acc += raw_at(a, raw, nrg, i + t);
+      out[i] = acc * a.pool_inv;
+    }
+    return;
   }
-  a.s_key[(int64_t)seg * a.n_tot + n0 + i] = acc * a.pool_inv;
+  for (int t = threadIdx.x; t < kPoolTile + 2 * half; t += 256) {
+    const int64_t j = i0 - half + t;
+    buf[t] = (j >= 0 && j < nb) ? raw_at(a, raw, nrg, j) : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kPoolTile / 256; ++u) {
+    const int l = threadIdx.x + 256 * u;
+    if (i0 + l >= nb) break;
+    float acc = 0.f;
+    for (int t = 0; t <= 2 * half; ++t) acc += buf[l + t];
+    out[i0 + l] = acc * a.pool_inv;
+  }
 }
 
 template <int D, int NP>
@@ -528,7 +561,7 @@ hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStre
   e = hipGetLastError();
   if (e == hipSuccess && ev) e = hipEventRecord(ev[2], stream);
   if (e != hipSuccess) return e;
-  const dim3 pgrid((unsigned)((max_nb + 255) / 256), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
+  const dim3 pgrid((unsigned)((max_nb + kPoolTile - 1) / kPoolTile), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
   hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e == hipSuccess && ev) e = hipEventRecord(ev[3], stream);

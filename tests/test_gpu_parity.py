@@ -204,6 +204,9 @@ GUIDE_CASES = [
     ("mha-g1-pool1", 1, 4, 4, 64, [777], [1], synth.DIST_NORMAL, 1),
     ("heavy-tail-outliers", 1, 8, 2, 128, [4500], [64], synth.DIST_STUDENT_T3, 7),
     ("pool-wider-than-seq", 1, 2, 1, 64, [1, 2, 3], [2, 1, 5], synth.DIST_NORMAL, 9),
+    ("chunk-edges", 1, 8, 2, 128, [8191, 8192, 8193, 16385], [64, 9, 64, 33], synth.DIST_NORMAL, 5),
+    ("wide-pool-staged", 1, 2, 1, 64, [2500, 40], [4, 2], synth.DIST_NORMAL, 1025),
+    ("wide-pool-direct", 1, 2, 1, 64, [3000], [4], synth.DIST_NORMAL, 1027),
 ]
 
 
