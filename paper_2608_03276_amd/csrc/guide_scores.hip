@@ -155,6 +155,22 @@ __device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) 
   }
 }
 
+// Issue-priority balancing of the two waves that share a SIMD (waves w and w ^ 4).  With equal
+// priority the older wave wins most issue slots, finishes its sub-tiles early and leaves
+// the other to run alone at the end of the workgroup.  After each sub-tile a wave publishes
+// its count and raises its priority while it is behind its partner.  This changes only the
+// timing, never which wave computes what.
+__device__ inline void balance_issue(int* progress, int wave, int done) {
+  if ((threadIdx.x & 63) == 0) progress[wave] = done;
+  const int other = uniform(progress[wave ^ 4]);
+  if (done < other)
+    __builtin_amdgcn_s_setprio(2);
+  else if (done == other)
+    __builtin_amdgcn_s_setprio(1);
+  else
+    __builtin_amdgcn_s_setprio(0);
+}
+
 // The staging buffer has landed (the wave's copies are complete).  The memory clobber keeps
 // the compiler from moving LDS reads of the buffer above the wait.
 __device__ inline void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -323,13 +339,18 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_stats(GuideArgs a) {
   for (int i = 0; i < 16; ++i) p0[i] = p1[i] = -INFINITY;  // empty pipeline slot
   read_qfrag<D>(qs, 0, qa);
   read_qfrag<D>(qs, 1, qb);
-  for (; st < nfull; st += kGuideWaves) {
+  __shared__ int progress[kGuideWaves];
+  if (threadIdx.x < kGuideWaves) progress[threadIdx.x] = 0;
+  __syncthreads();
+  for (int done = 0; st < nfull; st += kGuideWaves) {
     wait_copies();
     read_kfrag<D>(kbuf, kf);
     wait_lds_reads();
     if (st + kGuideWaves < nfull) dma_subtile<D>(kchunk, 32 * (st + kGuideWaves), ntok, kbuf);
     stats_steps<D, NP>(qs, kf, qa, qb, p0, p1, sm, ss, a.c);
+    balance_issue(progress, wave, ++done);
   }
+  __builtin_amdgcn_s_setprio(0);
   stats_update(p0, a.c, sm[NB - 2], ss[NB - 2]);
   stats_update(p1, a.c, sm[NB - 1], ss[NB - 1]);
   if (ntok > 32 * nfull && wave == nfull % kGuideWaves) {
@@ -479,14 +500,19 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
   int prev = -1;  // first chunk token of the sub-tile in the vector stage (none yet)
   read_qfrag<D>(qs, 0, qa);
   read_qfrag<D>(qs, 1, qb);
-  for (; st < nsub; st += kGuideWaves) {
+  __shared__ int progress[kGuideWaves];
+  if (threadIdx.x < kGuideWaves) progress[threadIdx.x] = 0;
+  __syncthreads();
+  for (int done = 0; st < nsub; st += kGuideWaves) {
     wait_copies();
     read_kfrag<D>(kbuf, kf);
     wait_lds_reads();
     if (st + kGuideWaves < nsub) dma_subtile<D>(kchunk, 32 * (st + kGuideWaves), ntok, kbuf);
     attn_steps<D, NP>(qs, lz_s, kf, qa, qb, p0, p1, part, prev, raw_out, ntok, a.c);
     prev = 32 * st;
+    balance_issue(progress, wave, ++done);
   }
+  __builtin_amdgcn_s_setprio(0);
   part += attn_sum(p0, a.c) + attn_sum(p1, a.c);
   attn_flush(part, raw_out, prev, ntok);
 }
