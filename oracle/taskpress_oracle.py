@@ -24,8 +24,10 @@ Sections cited are those of the paper:
   Sec. 6 (limitations)  the attention used is softmax-normalised.
 
 Readings where the paper is silent (each listed in the design notes):
-  - softmax over the context keys only (the guide's own keys are not in the
-    normaliser), logits scaled by `softmax_scale`;
+  - by default the softmax runs over the context keys only (the guide's own keys
+    are not in the normaliser); given the guide keys, it is the paper-literal
+    context slice of the causal attention over context + appended guide
+    (Sec. 3.2); logits scaled by `softmax_scale`;
   - the R query heads of a GQA group are averaged;
   - pooling pads with zeros outside [0, N) and always divides by K;
   - gamma stored as fp32; q = clamp(RNE(fl32(v / gamma)), +-qmax); gamma = 0
@@ -127,24 +129,38 @@ def keep_count(n: int, keep_ratio: float | None = None, keep_budget: int | None 
 
 
 # --------------------------------------------------------------------------- stage 1
-def attention_slice(q_rows: np.ndarray, k_rows: np.ndarray, softmax_scale: float) -> np.ndarray:
+def attention_slice(q_rows: np.ndarray, k_rows: np.ndarray, softmax_scale: float,
+                    kg_rows: np.ndarray | None = None) -> np.ndarray:
     """A[j, i]: attention weight of guide token j on context token i (Sec. 3.2).
 
-    Softmax-normalised (Sec. 6) over the N context keys of the segment, of the logits
-    softmax_scale * <q_j, k_i>.  q_rows [G, d], k_rows [N, d], float64."""
+    Softmax-normalised (Sec. 6) attention of the logits softmax_scale * <q_j, k_i>.
+    q_rows [G, d], k_rows [N, d], float64.  Without kg_rows the normaliser runs over the N
+    context keys only (the default reading).  With kg_rows [G, d], the guide's own keys,
+    A is the context slice of the full causal attention map of Sec. 3.2 with the guide
+    appended after the context: row j's normaliser also covers guide keys 0..j."""
     x = softmax_scale * (q_rows @ k_rows.T)
-    x = x - x.max(axis=1, keepdims=True)
-    e = np.exp(x)
-    return e / e.sum(axis=1, keepdims=True)
+    if kg_rows is None:
+        m = x.max(axis=1, keepdims=True)
+        e = np.exp(x - m)
+        return e / e.sum(axis=1, keepdims=True)
+    g = q_rows.shape[0]
+    y = softmax_scale * (q_rows @ kg_rows.T)                      # [G, G] guide-key logits
+    causal = np.arange(g)[None, :] <= np.arange(g)[:, None]        # key t visible to row j iff t <= j
+    y = np.where(causal, y, -np.inf)
+    m = np.maximum(x.max(axis=1, keepdims=True), y.max(axis=1, keepdims=True))
+    e = np.exp(x - m)
+    z = e.sum(axis=1, keepdims=True) + np.exp(y - m).sum(axis=1, keepdims=True)
+    return e / z
 
 
-def guide_attention_sum(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float) -> np.ndarray:
+def guide_attention_sum(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float,
+                        kg_rows: np.ndarray | None = None) -> np.ndarray:
     """Inner sum of Eq. 1, sum_j A[j, i], averaged over the R query heads that share the
-    KV head.  q_group [R, G, d]."""
+    KV head.  q_group [R, G, d]; kg_rows: the KV head's guide keys [G, d] or None."""
     R = q_group.shape[0]
     raw = np.zeros(k_rows.shape[0], dtype=np.float64)
     for r in range(R):
-        raw += attention_slice(q_group[r], k_rows, softmax_scale).sum(axis=0)
+        raw += attention_slice(q_group[r], k_rows, softmax_scale, kg_rows).sum(axis=0)
     return raw / R
 
 
@@ -163,9 +179,10 @@ def avg_pool(raw: np.ndarray, pool_k: int) -> np.ndarray:
     return acc / pool_k
 
 
-def key_scores(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float, pool_k: int) -> np.ndarray:
+def key_scores(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float, pool_k: int,
+               kg_rows: np.ndarray | None = None) -> np.ndarray:
     """s_key of Eq. 1 for one KV head: pooled guide-attention sum (float64, [N])."""
-    return avg_pool(guide_attention_sum(q_group, k_rows, softmax_scale), pool_k)
+    return avg_pool(guide_attention_sum(q_group, k_rows, softmax_scale, kg_rows), pool_k)
 
 
 # --------------------------------------------------------------------------- stage 2
@@ -243,17 +260,19 @@ def compact(rows: np.ndarray, idx: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- full path
-def evict_segment(q_group_bits, k_bits, v_bits, *, softmax_scale, pool_k, qfmt, bits, rule, k):
+def evict_segment(q_group_bits, k_bits, v_bits, *, softmax_scale, pool_k, qfmt, bits, rule, k, kg_bits=None):
     """All four stages for one (sequence, layer, KV head).
 
-    q_group_bits [R, G, d], k_bits / v_bits [N, d] (bf16 bit patterns).  Returns a dict
+    q_group_bits [R, G, d], k_bits / v_bits [N, d] (bf16 bit patterns); kg_bits [G, d], the
+    KV head's guide keys (bf16 bits), or None for the context-only normaliser.  Returns a dict
     with s_key (float64), gamma (fp32), q (quantised values, unpacked), vq (packed
     bytes), S (fp32 combined score), idx (int32, ascending), and the compact rows
     k_c (bf16 bits), vq_c (bytes), gamma_c (fp32)."""
     qg = bf16_to_f64(q_group_bits)
     kr = bf16_to_f64(k_bits)
     vr = bf16_to_f64(v_bits)
-    s_key = key_scores(qg, kr, softmax_scale, pool_k)
+    kg = None if kg_bits is None else bf16_to_f64(kg_bits)
+    s_key = key_scores(qg, kr, softmax_scale, pool_k, kg)
     gamma = value_scales(vr, qfmt, bits)
     q = quantize_values(vr, gamma, qfmt, bits)
     vq = pack_codes(q, qfmt, bits)

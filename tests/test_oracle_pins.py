@@ -128,6 +128,72 @@ def test_attention_dilution():
         prev = cur
 
 
+# ----------------------------------------------------------------------------- stage 1, guide keys
+def _full_causal_map(q_ctx, k_ctx, q_guide, k_guide, scale):
+    """Brute force from Sec. 3.2's description: append the guide after the context, build
+    the full causal attention map of size (N+G) x (N+G), softmax every row over the keys it
+    may see, and return the guide rows' context columns (the slice A)."""
+    qa = np.concatenate([q_ctx, q_guide])
+    ka = np.concatenate([k_ctx, k_guide])
+    n_all = qa.shape[0]
+    out = np.zeros((n_all, n_all))
+    for p in range(n_all):
+        logits = [scale * float(np.dot(qa[p], ka[t])) for t in range(p + 1)]  # causal: keys 0..p
+        m = max(logits)
+        w = [math.exp(v - m) for v in logits]
+        z = math.fsum(w)
+        for t in range(p + 1):
+            out[p, t] = w[t] / z
+    n = q_ctx.shape[0]
+    return out[n:, :n]
+
+
+def test_guide_keys_match_the_full_causal_map():
+    """With the guide's keys, A is the context slice of the causal attention map of the
+    context with the guide appended (Sec. 3.2), checked by building that map."""
+    for N, G, d, scale in [(5, 3, 4, 0.7), (12, 6, 8, 0.35), (1, 4, 2, 1.1)]:
+        q_ctx = rng.standard_normal((N, d))
+        k_ctx = rng.standard_normal((N, d)) * 2
+        q_g = rng.standard_normal((G, d)) * 2
+        k_g = rng.standard_normal((G, d)) * 2
+        want = _full_causal_map(q_ctx, k_ctx, q_g, k_g, scale)
+        got = o.attention_slice(q_g, k_ctx, scale, k_g)
+        assert np.allclose(got, want, rtol=1e-12, atol=1e-15)
+
+
+def test_guide_keys_closed_form_and_mass():
+    """All logits equal (Q = 0): row j spreads its weight evenly over the N context keys and
+    the j+1 guide keys it sees, so A[j, i] = 1/(N + j + 1); the context mass of every row is
+    below 1 and the rest is the weight on the guide keys."""
+    N, G, d = 40, 7, 16
+    q = np.zeros((2, G, d))
+    k = rng.standard_normal((N, d))
+    kg = rng.standard_normal((G, d))
+    A = o.attention_slice(q[0], k, 0.5, kg)
+    for j in range(G):
+        assert np.allclose(A[j], 1.0 / (N + j + 1), rtol=1e-13)
+    raw = o.guide_attention_sum(q, k, 0.5, kg)
+    assert np.allclose(raw, sum(1.0 / (N + j + 1) for j in range(G)), rtol=1e-13)
+    q = rng.standard_normal((1, G, d)) * 2
+    A = o.attention_slice(q[0], k, 0.5, kg)
+    mass = A.sum(axis=1)
+    assert np.all(mass < 1.0) and np.all(mass > 0.0)
+
+
+def test_guide_keys_reduce_to_context_softmax():
+    """Guide keys whose logits lie 1000 below the context's leave A equal to the context-only
+    softmax: their weight underflows to exactly 0 in float64."""
+    N, G, d = 30, 5, 8
+    q = rng.standard_normal((G, d))
+    q[:, 0] = np.abs(q[:, 0]) + 1.0          # every guide query has a positive first component
+    k = rng.standard_normal((N, d))
+    kg = np.zeros((G, d))
+    kg[:, 0] = -4000.0                       # so every guide logit is <= -2000
+    y = 0.5 * (q @ kg.T)
+    assert np.all(y <= -2000)
+    assert np.array_equal(o.attention_slice(q, k, 0.5, kg), o.attention_slice(q, k, 0.5))
+
+
 # ----------------------------------------------------------------------------- stage 2
 ALL_POS_BF16 = np.arange(1, 0x7F80, dtype=np.uint16)  # every positive finite bf16
 
