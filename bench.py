@@ -138,6 +138,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_128k")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--guide-keys", action="store_true",
+                    help="paper-literal normaliser: include the appended guide's own keys")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
@@ -161,6 +163,7 @@ def main():
     w = W.ALL[args.workload]()
     torch.cuda.set_device(0)
     q, k, v = pu.device_inputs(w)
+    kg = pu.device_guide_keys(w) if args.guide_keys else None
     d = B.dims(w.L, w.Hq, w.Hkv, w.d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
     ko = B.kept_offsets_for(bt, w.keep_ratio or 0.0, w.keep_budget or 0)
@@ -170,7 +173,7 @@ def main():
     def step(ev=None):
         B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
                    w.keep_budget or 0, ko, bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c,
-                   bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev)
+                   bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev, k_guide=kg)
 
     for _ in range(args.warmup):
         step()
@@ -207,14 +210,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
-        "config": {"workload": w.describe(), "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
+        "config": {"workload": w.describe() + (", guide keys in the normaliser" if kg is not None else ""),
+                   "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
                    "context_tokens": w.n_tot, "guide_tokens": w.g_tot, "kept_per_head": ko[-1]},
         "roofline": roofline,
         "path_hbm": {"achieved": round(path_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(path_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": path_bytes},
         "stages_ms": {n: round(t, 4) for n, t in stage_ms.items()},
     }
-    del q, k, v, bufs
+    del q, k, v, kg, bufs
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

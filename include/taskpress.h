@@ -120,20 +120,25 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
 
 /*
  * Step 1 — key score of Eq. 1 (Sec. 3.2), for every (sequence b, layer l, KV head h):
- *   A^(r)[j][i] = softmax_i( softmax_scale * <q_guide[l][r][g0+j], k[l][h][n0+i]> )
- *                 over the N_b context tokens i of sequence b (softmax-normalised as
- *                 stated in Sec. 6; the guide's own keys are not part of the normaliser),
+ *   A^(r)[j][i] = exp(x_ji) / Z_j with x_ji = softmax_scale * <q_guide[l][r][g0+j], k[l][h][n0+i]>
+ *                 (softmax-normalised as stated in Sec. 6), where the normaliser Z_j is
+ *                 - k_guide == NULL: sum_i exp(x_ji) over the N_b context tokens of sequence b;
+ *                 - k_guide != NULL: that sum plus sum_{t<=j} exp(softmax_scale *
+ *                   <q_guide[l][r][g0+j], k_guide[l][h][g0+t]>), i.e. A is the context slice
+ *                   of the causal attention over the context with the guide appended after
+ *                   it (the slice of the full attention map described in Sec. 3.2),
  *   raw[i]      = (1/R) * sum over the R query heads r of KV head h, sum_{j<G_b} A^(r)[j][i],
  *   s_key[l][h][n0+i] = (1/pool_k) * sum_{|t| <= pool_k/2} raw[i+t], raw = 0 outside [0, N_b).
- * q_guide bf16 [L][Hq][G_tot][d], k bf16 [L][Hkv][N_tot][d], s_key fp32 [L][Hkv][N_tot] (out).
+ * q_guide bf16 [L][Hq][G_tot][d], k bf16 [L][Hkv][N_tot][d], k_guide bf16 [L][Hkv][G_tot][d]
+ * (the guide tokens' keys) or NULL, s_key fp32 [L][Hkv][N_tot] (out).
  * softmax_scale > 0 (callers pass 1/sqrt(d)); pool_k odd, >= 1.
  * workspace: device, >= tp_workspace_size(TP_FN_GUIDE_SCORES, ...) bytes, 256-byte aligned.
  * Errors: TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE,
  * TP_ERR_HIP.
  */
 tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void* q_guide,
-                          const void* k, float softmax_scale, int32_t pool_k, float* s_key,
-                          void* workspace, size_t ws_bytes, void* stream);
+                          const void* k, const void* k_guide, float softmax_scale, int32_t pool_k,
+                          float* s_key, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Step 2 — value score of Eq. 2 (Sec. 3.3), fused with per-token quantisation of V
@@ -214,8 +219,9 @@ typedef struct tp_profile {
  * Every argument is validated before anything is enqueued.  Errors as for the four calls.
  */
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                   const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits,
-                   int32_t rule, double keep_ratio, int64_t keep_budget, const int64_t* kept_offsets,
+                   const void* k_guide, const void* v, float softmax_scale, int32_t pool_k,
+                   int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio, int64_t keep_budget,
+                   const int64_t* kept_offsets,
                    float* s_key, float* scales, void* v_q, float* s_out, int32_t* kept_idx,
                    void* k_out, void* v_q_out, float* scales_out, void* workspace, size_t ws_bytes,
                    const tp_profile* profile, void* stream);

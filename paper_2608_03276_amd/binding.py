@@ -107,7 +107,7 @@ def load():
     lib.tp_workspace_size.restype = ctypes.c_int32
     lib.tp_workspace_size.argtypes = [ctypes.c_int32, pd, pb, ctypes.POINTER(ctypes.c_size_t)]
     lib.tp_guide_scores.restype = ctypes.c_int32
-    lib.tp_guide_scores.argtypes = [pd, pb, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
+    lib.tp_guide_scores.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
     lib.tp_quantize_v_scales.restype = ctypes.c_int32
     lib.tp_quantize_v_scales.argtypes = [pd, pb, P, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.tp_combine_select_topk.restype = ctypes.c_int32
@@ -116,7 +116,7 @@ def load():
     lib.tp_compact_kv.restype = ctypes.c_int32
     lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
     lib.tp_evict.restype = ctypes.c_int32
-    lib.tp_evict.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+    lib.tp_evict.argtypes = [pd, pb, P, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                              ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64, P, P, P, P, P, P, P, P, P,
                              ctypes.c_size_t, ctypes.POINTER(TpProfile), P]
     _lib = lib
@@ -175,12 +175,14 @@ def tp_workspace_size(fn: int, d: TpDims, batch: Batch) -> int:
 
 
 def tp_guide_scores(d: TpDims, batch: Batch, q_guide, k, softmax_scale: float, pool_k: int, s_key, workspace,
-                    stream=None):
+                    stream=None, k_guide=None):
+    """k_guide: the guide tokens' keys bf16 [L][Hkv][G_tot][d] (paper-literal normaliser) or None."""
     L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
     _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
     _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(k_guide, L * Hkv * batch.g_tot * D * 2, "k_guide")
     _need(s_key, L * Hkv * batch.n_tot * 4, "s_key")
-    _check(load().tp_guide_scores(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k),
+    _check(load().tp_guide_scores(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(k_guide),
                                   float(softmax_scale), int(pool_k), _ptr(s_key), _ptr(workspace),
                                   workspace.numel() * workspace.element_size() if workspace is not None else 0,
                                   _stream(stream)))
@@ -262,12 +264,12 @@ class EvictBuffers:
 
 def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
           rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0, bufs: EvictBuffers = None,
-          stream=None) -> EvictBuffers:
+          stream=None, k_guide=None) -> EvictBuffers:
     """Run the four steps on one stream; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
     ko = kept_offsets_for(batch, keep_ratio, keep_budget)
     if bufs is None:
         bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
-    tp_guide_scores(d, batch, q_guide, k, softmax_scale, pool_k, bufs.s_key, bufs.ws_guide, stream)
+    tp_guide_scores(d, batch, q_guide, k, softmax_scale, pool_k, bufs.s_key, bufs.ws_guide, stream, k_guide)
     tp_quantize_v_scales(d, batch, v, qfmt, bits, bufs.scales, bufs.v_q, stream)
     tp_combine_select_topk(d, batch, bufs.s_key, bufs.scales, rule, keep_ratio, keep_budget, ko, bufs.kept_idx,
                            bufs.s_comb, None, stream)
@@ -278,7 +280,7 @@ def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_
 
 def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
              rule: int, keep_ratio: float, keep_budget: int, kept_offsets, s_key, scales, v_q, s_out, kept_idx,
-             k_out, v_q_out, scales_out, workspace, events=None, stream=None):
+             k_out, v_q_out, scales_out, workspace, events=None, stream=None, k_guide=None):
     """The whole path in one call.  `events`: None, or TP_EVICT_EVENTS torch.cuda.Event objects
     (enable_timing=True) that the library records between its kernels."""
     L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
@@ -286,6 +288,7 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
     _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
     _need(k, L * Hkv * n * D * 2, "k")
     _need(v, L * Hkv * n * D * 2, "v")
+    _need(k_guide, L * Hkv * batch.g_tot * D * 2, "k_guide")
     for t, nbytes, name in ((s_key, L * Hkv * n * 4, "s_key"), (scales, L * Hkv * n * 4, "scales"),
                             (v_q, L * Hkv * n * row_bytes(qfmt, bits, D), "v_q")):
         _need(t, nbytes, name)
@@ -302,7 +305,7 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
             handles.append(e.cuda_event)
         prof = TpProfile(TP_EVICT_EVENTS, (ctypes.c_void_p * TP_EVICT_EVENTS)(*handles))
     ws = workspace
-    _check(load().tp_evict(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(v),
+    _check(load().tp_evict(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(k_guide), _ptr(v),
                            float(softmax_scale), int(pool_k), int(qfmt), int(bits), int(rule), float(keep_ratio),
                            int(keep_budget), ko, _ptr(s_key), _ptr(scales), _ptr(v_q), _ptr(s_out),
                            _ptr(kept_idx), _ptr(k_out), _ptr(v_q_out), _ptr(scales_out), _ptr(ws),
@@ -311,12 +314,12 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
 
 def evict_fused(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int,
                 bits: int, rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0,
-                bufs: EvictBuffers = None, events=None, stream=None) -> EvictBuffers:
+                bufs: EvictBuffers = None, events=None, stream=None, k_guide=None) -> EvictBuffers:
     """The whole path through tp_evict; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
     ko = kept_offsets_for(batch, keep_ratio, keep_budget)
     if bufs is None:
         bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
     tp_evict(d, batch, q_guide, k, v, softmax_scale, pool_k, qfmt, bits, rule, keep_ratio, keep_budget, ko,
              bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c, bufs.v_q_c, bufs.scales_c,
-             bufs.ws_evict, events, stream)
+             bufs.ws_evict, events, stream, k_guide)
     return bufs

@@ -110,14 +110,14 @@ tp_status check_qfmt(int32_t qfmt, int32_t bits) {
 // enqueueing anything, so the fused entry point can validate every step before launching.
 
 tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                        float softmax_scale, int32_t pool_k, float* s_key, void* workspace, size_t ws_bytes,
-                        tp::GuideArgs& a) {
+                        const void* k_guide, float softmax_scale, int32_t pool_k, float* s_key, void* workspace,
+                        size_t ws_bytes, tp::GuideArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
   s = check_batch(batch, true);
   if (s != TP_OK) return s;
   if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
-  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key))
+  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key) || (k_guide && !aligned16(k_guide)))
     return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
   if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
     return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
@@ -138,6 +138,7 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   }
   a.q = (const uint16_t*)q_guide;
   a.k = (const uint16_t*)k;
+  a.kg = (const uint16_t*)k_guide;
   a.s_key = s_key;
   a.stats = (float2*)((char*)workspace + lay.stats_off);
   a.lse2 = (float*)((char*)workspace + lay.lse_off);
@@ -337,10 +338,11 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
 }
 
 tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                          float softmax_scale, int32_t pool_k, float* s_key, void* workspace,
-                          size_t ws_bytes, void* stream) {
+                          const void* k_guide, float softmax_scale, int32_t pool_k, float* s_key,
+                          void* workspace, size_t ws_bytes, void* stream) {
   tp::GuideArgs a;
-  const tp_status s = prepare_guide(dims, batch, q_guide, k, softmax_scale, pool_k, s_key, workspace, ws_bytes, a);
+  const tp_status s =
+      prepare_guide(dims, batch, q_guide, k, k_guide, softmax_scale, pool_k, s_key, workspace, ws_bytes, a);
   if (s != TP_OK) return s;
   const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream, nullptr);
   if (e != hipSuccess) return hip_fail(e, "tp_guide_scores launch");
@@ -382,8 +384,8 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
   return ok();
 }
 
-tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k, const void* v,
-                   float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
+tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                   const void* k_guide, const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
                    int64_t keep_budget, const int64_t* kept_offsets, float* s_key, float* scales, void* v_q,
                    float* s_out, int32_t* kept_idx, void* k_out, void* v_q_out, float* scales_out, void* workspace,
                    size_t ws_bytes, const tp_profile* profile, void* stream) {
@@ -402,7 +404,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   const size_t gws = guide_workspace_bytes(dims, batch);
   if (!workspace || ws_bytes < gws) return fail(TP_ERR_WORKSPACE, "workspace needs at least %zu bytes", gws);
   tp::GuideArgs ga;
-  s = prepare_guide(dims, batch, q_guide, k, softmax_scale, pool_k, s_key, workspace, gws, ga);
+  s = prepare_guide(dims, batch, q_guide, k, k_guide, softmax_scale, pool_k, s_key, workspace, gws, ga);
   if (s != TP_OK) return s;
   tp::QuantArgs qa;
   s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);

@@ -381,6 +381,45 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_stats(GuideArgs a) {
 }
 
 // ---------------------------------------------------------------------------- lse merge
+// One thread per guide row: merge the row's per-chunk (max, sum) pairs into lse2.  With the
+// guide's own keys (the paper-literal slice of the causal attention over context + appended
+// guide, Sec. 3.2), row j's normaliser also takes the logits of guide keys 0..j, computed
+// here (d products per key, fp32).
+template <int D>
+__device__ inline void guide_key_terms(const GuideArgs& a, int64_t grow, int64_t l, int64_t qh, int64_t g0, int64_t j,
+                                       float& m, float& s) {
+  const int64_t h = qh / a.R;
+  const uint4* qrow = (const uint4*)(a.q + grow * D);
+  float qf[D];
+#pragma unroll
+  for (int p = 0; p < D / 8; ++p) {
+    const uint4 u = qrow[p];
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qf[8 * p + 2 * e] = __uint_as_float(w[e] << 16);
+      qf[8 * p + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+  const uint16_t* kg = a.kg + ((l * a.Hkv + h) * a.g_tot + g0) * D;
+  for (int64_t t = 0; t <= j; ++t) {
+    const uint4* krow = (const uint4*)(kg + t * D);
+    float dot = 0.f;
+#pragma unroll
+    for (int p = 0; p < D / 8; ++p) {
+      const uint4 u = krow[p];
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dot = fmaf(qf[8 * p + 2 * e], __uint_as_float(w[e] << 16), dot);
+        dot = fmaf(qf[8 * p + 2 * e + 1], __uint_as_float(w[e] & 0xFFFF0000u), dot);
+      }
+    }
+    merge_stats(m, s, dot * a.c, 1.0f);
+  }
+}
+
+template <int D>
 __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
   const int b = blockIdx.y;
   const int64_t g0 = a.bt.g_off[b];
@@ -399,6 +438,7 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
     const float2 v = a.stats[(int64_t)c * growtot + grow];
     merge_stats(m, s, v.x, v.y);
   }
+  if (a.kg != nullptr) guide_key_terms<D>(a, grow, l, qh, g0, j, m, s);
   a.lse2[grow] = m + log2f(s);
 }
 
@@ -579,7 +619,7 @@ hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStre
   if (e == hipSuccess && ev) e = hipEventRecord(ev[0], stream);
   if (e != hipSuccess) return e;
   const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_lse, lgrid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(k_guide_lse<D>, lgrid, dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
   if (e != hipSuccess) return e;

@@ -25,9 +25,10 @@ constexpr int kChunkTokens = 8192;       // tokens of one segment per workgroup
 struct GuideArgs {
   const uint16_t* q;  // bf16 [L][Hq][G_tot][d]
   const uint16_t* k;  // bf16 [L][Hkv][N_tot][d]
+  const uint16_t* kg; // bf16 [L][Hkv][G_tot][d] guide keys, or nullptr (context-only normaliser)
   float* s_key;       // fp32 [L][Hkv][N_tot]
   float2* stats;      // [nchunk_max][L*Hq*G_tot]   per-chunk (max, sum) in the log2 domain
-  float* lse2;        // [L*Hq*G_tot]               log2-sum-exp2 of scaled logits per row
+  float* lse2;        // [L*Hq*G_tot]               log2-sum-exp2 of the row's normaliser
   float* raw;         // [nrg_max][L*Hkv][N_tot]    per row-group sums of normalised attention
   int32_t L, Hq, Hkv, R;
   int64_t n_tot, g_tot;

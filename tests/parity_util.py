@@ -40,6 +40,24 @@ def device_inputs(w, device="cuda"):
     return q, k, v
 
 
+def guide_key_stream(w):
+    """The guide tokens' keys of workload w (N(0,1), same seed as its guide queries)."""
+    return synth.Stream(w.q.seed, synth.TAG_KG)
+
+
+def device_guide_keys(w, device="cuda"):
+    """k_guide bf16 [L][Hkv][G_tot][d] of workload w, drawn on the GPU."""
+    kg = torch.empty(w.L * w.Hkv * w.g_tot * w.d, dtype=torch.bfloat16, device=device)
+    synth.device_fill(kg.data_ptr(), guide_key_stream(w), w.L, w.Hkv, list(w.guide_lens), w.d,
+                      torch.cuda.current_stream().cuda_stream)
+    return kg
+
+
+def host_guide_keys(w, b, l, h):
+    """bf16 bits of the guide keys of segment (b, l, h): [G_b, d]."""
+    return synth.rows(guide_key_stream(w), b, l, h, w.guide_lens[b], w.d)
+
+
 def host_segment(w, b, l, h):
     """bf16 bits of the oracle's inputs for segment (b, l, h): q_group [R, G_b, d], k, v [N_b, d]."""
     n, g = w.ctx_lens[b], w.guide_lens[b]
@@ -49,21 +67,22 @@ def host_segment(w, b, l, h):
     return qg, k, v
 
 
-def run_gpu(w, q, k, v, rule=None, bufs=None):
+def run_gpu(w, q, k, v, rule=None, bufs=None, k_guide=None):
     d = B.dims(w.L, w.Hq, w.Hkv, w.d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
     out = B.evict(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
                   rule=w.rule if rule is None else rule, keep_ratio=w.keep_ratio or 0.0,
-                  keep_budget=w.keep_budget or 0, bufs=bufs)
+                  keep_budget=w.keep_budget or 0, bufs=bufs, k_guide=k_guide)
     torch.cuda.synchronize()
     return out
 
 
-def oracle_segment(w, b, l, h, rule=None):
+def oracle_segment(w, b, l, h, rule=None, guide_keys=False):
     qg, kb, vb = host_segment(w, b, l, h)
     k = o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget)
     res = o.evict_segment(qg, kb, vb, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
-                          rule=w.rule if rule is None else rule, k=k)
+                          rule=w.rule if rule is None else rule, k=k,
+                          kg_bits=host_guide_keys(w, b, l, h) if guide_keys else None)
     res["k_bits"] = kb
     res["k"] = k
     return res
@@ -144,10 +163,10 @@ def assert_topk_of_own_scores(gpu_idx, gpu_S, what):
         assert kept_at_t.max() < evicted_at_t.min(), f"{what}: tie not broken towards the lower index"
 
 
-def check_segment(w, bufs, b, l, h, ref=None, rule=None):
+def check_segment(w, bufs, b, l, h, ref=None, rule=None, guide_keys=False):
     """Every output of segment (b, l, h) against the oracle; returns diagnostics."""
     if ref is None:
-        ref = oracle_segment(w, b, l, h, rule)
+        ref = oracle_segment(w, b, l, h, rule, guide_keys)
     g = seg_slice(w, bufs, b, l, h)
     tag = f"{w.name} seg(b={b},l={l},h={h})"
     err_s = assert_scores_close(g["s_key"], ref["s_key"], tag + " s_key")

@@ -69,9 +69,9 @@ def test_workspace_size():
     assert e.value.status == B.TP_ERR_PARAM
 
 
-def _gs(d, bt, q=FAKE, k=FAKE, scale=0.125, pool=5, s=FAKE, ws=FAKE, wsb=1 << 40):
-    return lib.tp_guide_scores(ctypes.byref(d), ctypes.byref(bt.c) if bt is not None else None, q, k, scale, pool,
-                               s, ws, wsb, None)
+def _gs(d, bt, q=FAKE, k=FAKE, scale=0.125, pool=5, s=FAKE, ws=FAKE, wsb=1 << 40, kg=None):
+    return lib.tp_guide_scores(ctypes.byref(d), ctypes.byref(bt.c) if bt is not None else None, q, k, kg, scale,
+                               pool, s, ws, wsb, None)
 
 
 @no_gpu
@@ -91,6 +91,7 @@ def test_guide_scores_validation():
         (dict(wsb=100), B.TP_ERR_WORKSPACE),
         (dict(ws=FAKE + 16), B.TP_ERR_WORKSPACE),
         (dict(q=FAKE + 2), B.TP_ERR_PARAM),
+        (dict(kg=FAKE + 8), B.TP_ERR_PARAM),
     ]
     for kw, want in cases:
         assert _gs(d, bt, **kw) == want, kw
@@ -103,7 +104,8 @@ def test_guide_scores_validation():
     assert _gs(d, B.Batch([1, 100, 300], [0, 16, 20])) == B.TP_ERR_SHAPE
     assert _gs(d, B.Batch([0, 100, 300])) == B.TP_ERR_NULL  # no guide offsets
     assert _gs(d, B.Batch(list(range(0, 66)), list(range(0, 66)))) == B.TP_ERR_UNSUPPORTED  # batch > 64
-    assert lib.tp_guide_scores(None, ctypes.byref(bt.c), FAKE, FAKE, 0.1, 1, FAKE, FAKE, 1 << 40, None) == B.TP_ERR_NULL
+    assert lib.tp_guide_scores(None, ctypes.byref(bt.c), FAKE, FAKE, None, 0.1, 1, FAKE, FAKE, 1 << 40,
+                               None) == B.TP_ERR_NULL
 
 
 @no_gpu
@@ -157,7 +159,7 @@ def test_compact_validation():
 
 
 def _ev(d, bt, **kw):
-    a = dict(q=FAKE, k=FAKE, v=FAKE, scale=0.125, pool=5, qfmt=0, bits=8, rule=0, ratio=0.25, budget=0,
+    a = dict(q=FAKE, k=FAKE, kg=None, v=FAKE, scale=0.125, pool=5, qfmt=0, bits=8, rule=0, ratio=0.25, budget=0,
              ko=None, skey=FAKE, sc=FAKE, vq=FAKE, sout=FAKE, idx=FAKE, kout=FAKE, vqout=FAKE, scout=FAKE,
              ws=FAKE, wsb=1 << 40, prof=None)
     a.update(kw)
@@ -165,7 +167,7 @@ def _ev(d, bt, **kw):
         a["ko"] = B.kept_offsets_for(bt, a["ratio"], a["budget"])
     ko = (ctypes.c_int64 * len(a["ko"]))(*a["ko"])
     prof = ctypes.byref(a["prof"]) if a["prof"] is not None else None
-    return lib.tp_evict(ctypes.byref(d), ctypes.byref(bt.c), a["q"], a["k"], a["v"], a["scale"], a["pool"],
+    return lib.tp_evict(ctypes.byref(d), ctypes.byref(bt.c), a["q"], a["k"], a["kg"], a["v"], a["scale"], a["pool"],
                         a["qfmt"], a["bits"], a["rule"], a["ratio"], a["budget"], ko, a["skey"], a["sc"], a["vq"],
                         a["sout"], a["idx"], a["kout"], a["vqout"], a["scout"], a["ws"], a["wsb"], prof, None)
 
@@ -196,6 +198,7 @@ def test_evict_validation():
         (dict(prof=short_prof), B.TP_ERR_PARAM),
         (dict(prof=null_prof), B.TP_ERR_NULL),
         (dict(k=FAKE + 8), B.TP_ERR_PARAM),
+        (dict(kg=FAKE + 4), B.TP_ERR_PARAM),
     ]
     for kw, want in cases:
         assert _ev(d, bt, **kw) == want, kw

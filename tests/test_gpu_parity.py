@@ -210,20 +210,20 @@ GUIDE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", GUIDE_CASES, ids=[c[0] for c in GUIDE_CASES])
-def test_guide_scores_parity(gpu_lib, case):
+def _guide_case(case, guide_keys):
     name, L, Hq, Hkv, d, lens, glens, dist, pool = case
-    pu.log(f"guide scores case {name}")
+    pu.log(f"guide scores case {name}{' with guide keys' if guide_keys else ''}")
     out_frac, out_scale = (0.02, 30.0) if dist == synth.DIST_STUDENT_T3 else (0.0, 1.0)
     w = W.Workload(name, L, Hq, Hkv, d, tuple(lens), tuple(glens), synth.Stream(61, synth.TAG_Q),
                    synth.Stream(61, synth.TAG_K, dist, out_frac, out_scale), synth.Stream(61, synth.TAG_V),
                    keep_ratio=0.25, pool_k=pool)
     q, k, v = pu.device_inputs(w)
+    kg = pu.device_guide_keys(w) if guide_keys else None
     dd = B.dims(L, Hq, Hkv, d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
     s_key = torch.empty(L * Hkv * w.n_tot, dtype=torch.float32, device="cuda")
     ws = torch.empty(B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, dd, bt), dtype=torch.uint8, device="cuda")
-    B.tp_guide_scores(dd, bt, q, k, w.softmax_scale, pool, s_key, ws)
+    B.tp_guide_scores(dd, bt, q, k, w.softmax_scale, pool, s_key, ws, k_guide=kg)
     torch.cuda.synchronize()
     got = s_key.cpu().numpy().reshape(L * Hkv, w.n_tot)
     offs = w.ctx_offsets()
@@ -232,10 +232,22 @@ def test_guide_scores_parity(gpu_lib, case):
         for l in range(L):
             for h in range(Hkv):
                 qg, kb, _ = pu.host_segment(w, b, l, h)
-                ref = o.key_scores(o.bf16_to_f64(qg), o.bf16_to_f64(kb), w.softmax_scale, pool)
+                kgr = o.bf16_to_f64(pu.host_guide_keys(w, b, l, h)) if guide_keys else None
+                ref = o.key_scores(o.bf16_to_f64(qg), o.bf16_to_f64(kb), w.softmax_scale, pool, kgr)
                 worst = max(worst, pu.assert_scores_close(got[l * Hkv + h, offs[b]:offs[b + 1]], ref,
                                                           f"{name} b={b} l={l} h={h}"))
     pu.log(f"  max rel err {worst:.3g}")
+
+
+@pytest.mark.parametrize("case", GUIDE_CASES, ids=[c[0] for c in GUIDE_CASES])
+def test_guide_scores_parity(gpu_lib, case):
+    _guide_case(case, False)
+
+
+@pytest.mark.parametrize("case", GUIDE_CASES[:5], ids=[c[0] for c in GUIDE_CASES[:5]])
+def test_guide_scores_with_guide_keys(gpu_lib, case):
+    """The paper-literal normaliser (guide keys 0..j of the appended guide included)."""
+    _guide_case(case, True)
 
 
 # ----------------------------------------------------------------------------- whole path
@@ -313,6 +325,25 @@ def test_evict_against_oracle(gpu_lib):
     for b in range(w.batch):
         for h in range(w.Hkv):
             pu.check_segment(w, bufs, b, 0, h)
+
+
+def test_evict_with_guide_keys_against_oracle(gpu_lib):
+    w = W.ragged8().with_(name="ragged-guide-keys", L=2, ctx_lens=(3000, 1, 700), guide_lens=(32, 5, 128),
+                          keep_budget=300)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    q, k, v = pu.device_inputs(w)
+    kg = pu.device_guide_keys(w)
+    bufs = B.evict_fused(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                         rule=w.rule, keep_budget=w.keep_budget, k_guide=kg)
+    torch.cuda.synchronize()
+    for b in range(w.batch):
+        for l in range(w.L):
+            for h in (0, w.Hkv - 1):
+                pu.check_segment(w, bufs, b, l, h, guide_keys=True)
+    # the guide keys change the scores (the context mass of a row drops below 1)
+    plain = pu.run_gpu(w, q, k, v)
+    assert not torch.equal(plain.s_key, bufs.s_key)
 
 
 def test_evict_profile_events(gpu_lib):
