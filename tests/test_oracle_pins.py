@@ -228,6 +228,25 @@ def test_quant_int_exhaustive_at_unit_absmax():
     assert np.all(err <= g[:, None].astype(np.float64) * (0.5 + 1e-6))
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+def test_quant_int_quotient_rounded_to_fp32_first(bits):
+    """q = RNE(fl32(v / gamma)): the quotient is rounded to fp32 before the integer rounding.
+    For every bf16 absmax in [1, 2) and every bf16 v in [0, absmax] the codes equal numpy's
+    IEEE fp32 division followed by RNE; this sweep includes the v = absmax/2 cases whose fp32
+    quotient lands exactly on a half while the exact quotient does not."""
+    qm = 2 ** (bits - 1) - 1
+    pos = o.bf16_to_f64(np.arange(0, 0x7F80, dtype=np.uint16))
+    for a_bits in range(0x3F80, 0x4000):
+        a = float(o.bf16_to_f64(np.array([a_bits], dtype=np.uint16))[0])
+        v = pos[pos <= a]
+        rows = np.stack([np.full(v.shape, a), v], axis=1)
+        g = o.value_scales(rows, o.QFMT_INT, bits)
+        q = o.quantize_values(rows, g, o.QFMT_INT, bits)
+        y32 = v.astype(np.float32) / g.astype(np.float32)
+        ref = np.clip(np.rint(y32.astype(np.float64)), -qm, qm).astype(np.int8)
+        assert np.array_equal(q[:, 1], ref), a
+
+
 @pytest.mark.parametrize("qfmt,bits", [(o.QFMT_INT, 8), (o.QFMT_INT, 4), (o.QFMT_FP8_E4M3, 8)])
 def test_quant_properties(qfmt, bits):
     """The absmax element maps to +-qmax; scaling a row by 2^e leaves q unchanged and scales
