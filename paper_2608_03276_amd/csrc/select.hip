@@ -19,6 +19,7 @@ namespace {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kPerThread = 4;
+constexpr int kBatch = 8;  // keys each thread loads before it touches the histogram
 
 __device__ inline uint32_t order_key(float s) {
   uint32_t b = __float_as_uint(s);
@@ -118,10 +119,24 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
 
   for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
   __syncthreads();
-  for (int64_t i = tid; i < nb; i += kSelThreads) {
-    const float S = combine(a.rule, sk[i], sc[i], norm_a, norm_b);
-    sb[i] = S;
-    atomicAdd(&hist[order_key(S) >> 24], 1u);
+  // batches of kBatch keys per thread: the loads of a batch are in flight together
+  for (int64_t i0 = 0; i0 < nb; i0 += (int64_t)kSelThreads * kBatch) {
+    float x[kBatch], y[kBatch];
+#pragma unroll
+    for (int e = 0; e < kBatch; ++e) {
+      const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+      x[e] = i < nb ? sk[i] : 0.f;
+      y[e] = i < nb ? sc[i] : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < kBatch; ++e) {
+      const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+      if (i < nb) {
+        const float S = combine(a.rule, x[e], y[e], norm_a, norm_b);
+        sb[i] = S;
+        atomicAdd(&hist[order_key(S) >> 24], 1u);
+      }
+    }
   }
   __syncthreads();
 
@@ -131,9 +146,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     if (pass > 0) {
       for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
       __syncthreads();
-      for (int64_t i = tid; i < nb; i += kSelThreads) {
-        const uint32_t key = order_key(sb[i]);
-        if ((key >> (shift + 8)) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      for (int64_t i0 = 0; i0 < nb; i0 += (int64_t)kSelThreads * kBatch) {
+        float x[kBatch];
+#pragma unroll
+        for (int e = 0; e < kBatch; ++e) {
+          const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+          x[e] = i < nb ? sb[i] : 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < kBatch; ++e) {
+          const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+          const uint32_t key = order_key(x[e]);
+          if (i < nb && (key >> (shift + 8)) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
       }
       __syncthreads();
     }
