@@ -60,6 +60,40 @@ __device__ inline uint32_t e4m3_code(float y) {
   return sign | code;
 }
 
+// Codes of 8 values in the normalised domain (the quotient y of each, then the format's code).
+// ys = 1/gs, sc = 2^-e; valid when the absmax exponent field exceeds 27.
+__device__ inline void codes_scaled(const uint32_t (&w)[4], float sc, float gs, float ys, const QuantFmt& f,
+                                    uint32_t (&code)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float v = __uint_as_float(h);
+    const float vs = v * sc;
+    const float q0 = vs * ys;
+    const float y = fmaf(fmaf(-q0, gs, vs), ys, q0);
+    if (f.int_fmt)
+      code[i] = (uint32_t)(int32_t)__builtin_amdgcn_fmed3f(__builtin_rintf(y), -f.qmax, f.qmax);
+    else
+      code[i] = e4m3_code(__builtin_copysignf(y, v));
+  }
+}
+
+// Codes by IEEE division (rows with a tiny or zero absmax).
+__device__ inline void codes_divided(const uint32_t (&w)[4], float gamma, const QuantFmt& f, uint32_t (&code)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float v = __uint_as_float(h);
+    const float y = v / gamma;
+    if (gamma == 0.0f)
+      code[i] = 0;
+    else if (f.int_fmt)
+      code[i] = (uint32_t)(int32_t)__builtin_amdgcn_fmed3f(__builtin_rintf(y), -f.qmax, f.qmax);
+    else
+      code[i] = e4m3_code(__builtin_copysignf(y, v));
+  }
+}
+
 // Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
 // LPT consecutive lanes; every lane of the wave must call this together (the absmax is
 // reduced across lanes).  Returns gamma (the same on all LPT lanes of the row) and the
@@ -69,40 +103,24 @@ __device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& ou
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   uint32_t mx = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    mx = max(mx, w[i] & 0x7FFFu);
-    mx = max(mx, (w[i] >> 16) & 0x7FFFu);
-  }
+  for (int i = 0; i < 4; ++i) mx = max(mx, max(w[i] & 0x7FFFu, (w[i] >> 16) & 0x7FFFu));
   mx = group_max<LPT>(mx);
   const float amax = __uint_as_float(mx << 16);
   const float gamma = amax / f.qmax;
-  // exponent field of the absmax (bf16 and fp32 share it); below 2^-100 divide directly
+  // exponent field of the absmax (bf16 and fp32 share it); below 2^-100 (zero rows
+  // included) the division path is taken, for the whole wave when any lane needs it
   const int ef = (int)(mx >> 7);
-  const bool direct = ef <= 27;
-  const float sc = direct ? 1.0f : __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
-  const float gs = gamma * sc;
-  const float ys = 1.0f / gs;
   uint32_t code[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const uint32_t h = (i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xFFFFu);
-    const float v = __uint_as_float(h << 16);
-    float y;
-    if (direct) {
-      y = v / gamma;
-    } else {
-      const float vs = v * sc;
-      const float q0 = vs * ys;
-      y = fmaf(fmaf(-q0, gs, vs), ys, q0);
-    }
-    if (gamma == 0.0f) {
-      code[i] = 0;
-    } else if (f.int_fmt) {
-      const float r = __builtin_amdgcn_fmed3f(__builtin_rintf(y), -f.qmax, f.qmax);
-      code[i] = (uint32_t)(int32_t)r;
-    } else {
-      code[i] = e4m3_code(__builtin_copysignf(y, v));
-    }
+  if (__builtin_amdgcn_ballot_w64(ef <= 27) == 0) {
+    const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+    const float gs = gamma * sc;
+    codes_scaled(w, sc, gs, 1.0f / gs, f, code);
+  } else if (ef <= 27) {
+    codes_divided(w, gamma, f, code);
+  } else {
+    const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+    const float gs = gamma * sc;
+    codes_scaled(w, sc, gs, 1.0f / gs, f, code);
   }
   if (f.nibbles) {
     uint32_t p = 0;
@@ -111,20 +129,30 @@ __device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& ou
     out.x = p;
     out.y = 0;
   } else {
-    out.x = (code[0] & 0xFFu) | ((code[1] & 0xFFu) << 8) | ((code[2] & 0xFFu) << 16) | ((code[3] & 0xFFu) << 24);
-    out.y = (code[4] & 0xFFu) | ((code[5] & 0xFFu) << 8) | ((code[6] & 0xFFu) << 16) | ((code[7] & 0xFFu) << 24);
+    // bytes 0 of (c0, c1, c2, c3) -> one dword, via two byte permutes and a word merge
+    const uint32_t lo01 = __builtin_amdgcn_perm(code[1], code[0], 0x0c0c0400u);
+    const uint32_t lo23 = __builtin_amdgcn_perm(code[3], code[2], 0x0c0c0400u);
+    const uint32_t hi01 = __builtin_amdgcn_perm(code[5], code[4], 0x0c0c0400u);
+    const uint32_t hi23 = __builtin_amdgcn_perm(code[7], code[6], 0x0c0c0400u);
+    out.x = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
+    out.y = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
   }
   return gamma;
 }
 
 // Store the codes of one piece: row `row` of a code tensor with `row_bytes` per row, piece
-// `sub` (D/8 pieces per row).
+// `sub` (D/8 pieces per row).  Nontemporal: the codes are streamed out, not re-read here.
 template <int D>
 __device__ inline void store_codes(uint8_t* vq, int64_t row, int sub, const QuantFmt& f, const uint2& c) {
-  if (f.nibbles)
-    *((uint32_t*)(vq + row * (D / 2)) + sub) = c.x;
-  else
-    *((uint2*)(vq + row * D) + sub) = c;
+  typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+  if (f.nibbles) {
+    __builtin_nontemporal_store(c.x, (uint32_t*)(vq + row * (D / 2)) + sub);
+  } else {
+    u32x2 t;
+    t.x = c.x;
+    t.y = c.y;
+    __builtin_nontemporal_store(t, (u32x2*)(vq + row * D) + sub);
+  }
 }
 
 }  // namespace tp

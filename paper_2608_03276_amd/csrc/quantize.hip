@@ -11,7 +11,7 @@ namespace {
 
 constexpr int kQuantThreads = 256;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 8;  // rows in flight per lane group
 
 template <int D>
 __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
