@@ -153,10 +153,17 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   a.pool_inv = (float)(1.0 / ((double)a.R * pool_k));
   a.pool_half = pool_k / 2;
   a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
-  a.nchunk_pad = (a.nchunk_max + 7) & ~7;
   a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
-  if ((int64_t)a.nchunk_pad * a.nrg_max > 0x7FFFFFFF)
-    return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
+  int64_t wg = 0;
+  a.wg_off[0] = 0;
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t gb = batch->guide_offsets[b + 1] - batch->guide_offsets[b];
+    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
+    wg += (units + 7) / 8 * 8 * ((a.R * gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
+    if (wg > 0x7FFFFFFF) return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
+    a.wg_off[b + 1] = (int32_t)wg;
+  }
   return TP_OK;
 }
 

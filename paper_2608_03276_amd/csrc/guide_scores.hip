@@ -55,28 +55,35 @@ struct Work {
 
 __device__ inline int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-// Workgroup -> (row group, chunk, segment, sequence).  Consecutive workgroup ids are dealt
-// round-robin to the 8 XCDs; the row groups of one chunk are given ids 8 apart so they land
-// on the same XCD and share the chunk's K through that XCD's L2.
+// Workgroup -> (sequence, row group, chunk, segment).  Each sequence owns a contiguous range
+// of workgroup ids (wg_off).  Within it the work units (segment, chunk) are numbered
+// consecutively and dealt round-robin to the 8 XCDs, as consecutive workgroup ids are, so
+// every XCD gets an even share whatever the number of chunks; the row groups of one unit get
+// ids 8 apart, so they land on the same XCD and share the chunk's K through its L2.
 __device__ inline bool decode(const GuideArgs& a, Work& w) {
   const int x = blockIdx.x;
-  const int xcd = x & 7, slot = x >> 3;
-  w.rg = slot % a.nrg_max;
-  w.chunk = xcd + 8 * (slot / a.nrg_max);
-  w.seg = blockIdx.y;
+  int b = 0;
+  while (b + 1 < a.bt.batch && x >= a.wg_off[b + 1]) ++b;
+  w.b = b;
+  const int xb = x - a.wg_off[b];
+  w.n0 = a.bt.ctx_off[b];
+  w.nb = a.bt.ctx_off[b + 1] - w.n0;
+  w.g0 = a.bt.g_off[b];
+  w.gb = (int)(a.bt.g_off[b + 1] - w.g0);
+  w.rows = a.R * w.gb;
+  const int nrg = (w.rows + kRowsPerGroup - 1) / kRowsPerGroup;
+  const int nchunk = (int)((w.nb + kChunkTokens - 1) / kChunkTokens);
+  const int xcd = xb & 7, slot = xb >> 3;
+  w.rg = slot % nrg;
+  const int64_t unit = (int64_t)(slot / nrg) * 8 + xcd;
+  if (unit >= (int64_t)a.L * a.Hkv * nchunk) return false;  // padding to a multiple of 8
+  w.seg = (int)(unit / nchunk);
+  w.chunk = (int)(unit % nchunk);
   w.l = w.seg / a.Hkv;
   w.h = w.seg % a.Hkv;
-  w.b = blockIdx.z;
-  w.n0 = a.bt.ctx_off[w.b];
-  w.nb = a.bt.ctx_off[w.b + 1] - w.n0;
   w.c0 = (int64_t)w.chunk * kChunkTokens;
-  if (w.c0 >= w.nb) return false;
   w.c1 = w.c0 + kChunkTokens < w.nb ? w.c0 + kChunkTokens : w.nb;
-  w.g0 = a.bt.g_off[w.b];
-  w.gb = (int)(a.bt.g_off[w.b + 1] - w.g0);
-  w.rows = a.R * w.gb;
   w.row0 = w.rg * kRowsPerGroup;
-  if (w.row0 >= w.rows) return false;
   w.nrows = w.rows - w.row0 < kRowsPerGroup ? w.rows - w.row0 : kRowsPerGroup;
   return true;
 }
@@ -611,48 +618,60 @@ __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
 }
 
 template <int D, int NP>
-hipError_t launch_np(const GuideArgs& a, int64_t max_nb, int64_t max_gb, hipStream_t stream, hipEvent_t* ev) {
-  const dim3 block(kGuideThreads);
-  const dim3 grid((unsigned)(a.nrg_max * a.nchunk_pad), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL((k_guide_stats<D, NP>), grid, block, 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[0], stream);
-  if (e != hipSuccess) return e;
-  const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_lse<D>, lgrid, dim3(256), 0, stream, a);
-  e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_guide_attn<D, NP>), grid, block, 0, stream, a);
-  e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[2], stream);
-  if (e != hipSuccess) return e;
-  const dim3 pgrid((unsigned)((max_nb + kPoolTile - 1) / kPoolTile), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
-  hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
-  e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[3], stream);
-  return e;
+hipError_t launch_pass(const GuideArgs& a, bool attn, hipStream_t stream) {
+  const unsigned nwg = (unsigned)a.wg_off[a.bt.batch];
+  if (nwg == 0) return hipSuccess;
+  if (attn)
+    hipLaunchKernelGGL((k_guide_attn<D, NP>), dim3(nwg), dim3(kGuideThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_guide_stats<D, NP>), dim3(nwg), dim3(kGuideThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
-// NP = row-block pairs a workgroup stages: enough for the largest row group, so short
-// guides do not pay for 256 rows.
+// One launch per class of sequences that need the same number NP of staged row-block pairs
+// (NP = ceil(min(R G_b, 256) / 64)), so short guides do not pay for 256 rows; each class's
+// arguments give the other sequences empty workgroup ranges.
 template <int D>
 hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
   static_assert(Cfg<D>::kSubPerWave >= 1, "chunk too small");
   int64_t max_nb = 0, max_gb = 0;
+  GuideArgs cls[4];
+  int64_t wg[4] = {0, 0, 0, 0};
+  for (int c = 0; c < 4; ++c) {
+    cls[c] = a;
+    cls[c].wg_off[0] = 0;
+  }
   for (int b = 0; b < a.bt.batch; ++b) {
     const int64_t nb = a.bt.ctx_off[b + 1] - a.bt.ctx_off[b];
     const int64_t gb = a.bt.g_off[b + 1] - a.bt.g_off[b];
     if (nb > max_nb) max_nb = nb;
     if (gb > max_gb) max_gb = gb;
+    const int64_t rows = (int64_t)a.R * gb;
+    const int np = (int)(((rows < kRowsPerGroup ? rows : kRowsPerGroup) + 63) / 64);
+    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + kChunkTokens - 1) / kChunkTokens);
+    wg[np - 1] += (units + 7) / 8 * 8 * ((rows + kRowsPerGroup - 1) / kRowsPerGroup);
+    for (int c = 0; c < 4; ++c) cls[c].wg_off[b + 1] = (int32_t)wg[c];
   }
-  const int64_t rows = (int64_t)a.R * max_gb < kRowsPerGroup ? (int64_t)a.R * max_gb : kRowsPerGroup;
-  switch ((rows + 63) / 64) {
-    case 1: return launch_np<D, 1>(a, max_nb, max_gb, stream, ev);
-    case 2: return launch_np<D, 2>(a, max_nb, max_gb, stream, ev);
-    case 3: return launch_np<D, 3>(a, max_nb, max_gb, stream, ev);
-    default: return launch_np<D, 4>(a, max_nb, max_gb, stream, ev);
+  for (int pass = 0; pass < 2; ++pass) {  // the large classes first: shorter tail
+    hipError_t e = launch_pass<D, 4>(cls[3], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 3>(cls[2], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 2>(cls[1], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 1>(cls[0], pass == 1, stream);
+    if (e == hipSuccess && ev) e = hipEventRecord(ev[pass == 0 ? 0 : 2], stream);
+    if (e != hipSuccess) return e;
+    if (pass == 0) {
+      const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
+      hipLaunchKernelGGL(k_guide_lse<D>, lgrid, dim3(256), 0, stream, a);
+      e = hipGetLastError();
+      if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
+      if (e != hipSuccess) return e;
+    }
   }
+  const dim3 pgrid((unsigned)((max_nb + kPoolTile - 1) / kPoolTile), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
+  hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[3], stream);
+  return e;
 }
 
 }  // namespace

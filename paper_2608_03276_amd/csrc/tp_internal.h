@@ -36,9 +36,11 @@ struct GuideArgs {
   float pool_inv;     // 1 / (R * pool_k)
   int32_t pool_half;  // pool_k / 2
   int32_t nchunk_max; // chunks of the longest sequence
-  int32_t nchunk_pad; // nchunk_max rounded up to a multiple of 8 (XCD count)
   int32_t nrg_max;    // row groups of the largest R * G_b
   BatchArgs bt;
+  // first workgroup of each sequence's range in the score passes: sequence b has
+  // ceil(L * Hkv * nchunk_b / 8) * 8 * nrg_b workgroups
+  int32_t wg_off[TP_MAX_BATCH + 1];
 };
 
 struct GuideWorkspace {

@@ -207,6 +207,8 @@ GUIDE_CASES = [
     ("chunk-edges", 1, 8, 2, 128, [8191, 8192, 8193, 16385], [64, 9, 64, 33], synth.DIST_NORMAL, 5),
     ("wide-pool-staged", 1, 2, 1, 64, [2500, 40], [4, 2], synth.DIST_NORMAL, 1025),
     ("wide-pool-direct", 1, 2, 1, 64, [3000], [4], synth.DIST_NORMAL, 1027),
+    # one launch per row-block class: 64, 128, 192 and 320 (= 256 + 64) guide rows
+    ("row-classes", 2, 8, 2, 128, [9000, 1500, 20000, 4097], [16, 32, 48, 80], synth.DIST_NORMAL, 5),
 ]
 
 
