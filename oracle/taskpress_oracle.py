@@ -164,6 +164,36 @@ def guide_attention_sum(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: 
     return raw / R
 
 
+def guide_log_normalisers(q_rows: np.ndarray, k_rows: np.ndarray, softmax_scale: float,
+                          kg_rows: np.ndarray | None = None) -> np.ndarray:
+    """ln of each guide row's softmax normaliser, ln sum over the row's keys of
+    exp(softmax_scale * <q_j, key>): over the N context keys, plus guide keys 0..j when
+    kg_rows is given (the causal map of Sec. 3.2).  This is the log-sum-exp a prefill
+    attention kernel reports for the appended guide rows.  q_rows [G, d] -> [G]."""
+    x = softmax_scale * (q_rows @ k_rows.T)
+    if kg_rows is not None:
+        g = q_rows.shape[0]
+        y = softmax_scale * (q_rows @ kg_rows.T)
+        y = np.where(np.arange(g)[None, :] <= np.arange(g)[:, None], y, -np.inf)
+        x = np.concatenate([x, y], axis=1)
+    m = x.max(axis=1)
+    return m + np.log(np.exp(x - m[:, None]).sum(axis=1))
+
+
+def guide_attention_sum_given_lse(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float,
+                                  lse: np.ndarray) -> np.ndarray:
+    """Inner sum of Eq. 1 with the normaliser supplied by the caller (Sec. 3.2 slices A from
+    the prefill's attention map, whose kernel already has each guide row's log-sum-exp):
+    A[j, i] = exp(softmax_scale * <q_j, k_i> - lse_j), summed over j and averaged over the
+    R query heads.  q_group [R, G, d], lse [R, G] (natural log)."""
+    R = q_group.shape[0]
+    raw = np.zeros(k_rows.shape[0], dtype=np.float64)
+    for r in range(R):
+        x = softmax_scale * (q_group[r] @ k_rows.T)
+        raw += np.exp(x - np.asarray(lse[r], dtype=np.float64)[:, None]).sum(axis=0)
+    return raw / R
+
+
 def avg_pool(raw: np.ndarray, pool_k: int) -> np.ndarray:
     """Outer part of Eq. 1: (1/K) sum_{t=-floor(K/2)}^{floor(K/2)} raw[i + t], with raw = 0
     outside [0, N).  K must be odd."""
@@ -183,6 +213,12 @@ def key_scores(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float, po
                kg_rows: np.ndarray | None = None) -> np.ndarray:
     """s_key of Eq. 1 for one KV head: pooled guide-attention sum (float64, [N])."""
     return avg_pool(guide_attention_sum(q_group, k_rows, softmax_scale, kg_rows), pool_k)
+
+
+def key_scores_given_lse(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float, pool_k: int,
+                         lse: np.ndarray) -> np.ndarray:
+    """s_key of Eq. 1 with the guide rows' log-normalisers supplied (float64, [N])."""
+    return avg_pool(guide_attention_sum_given_lse(q_group, k_rows, softmax_scale, lse), pool_k)
 
 
 # --------------------------------------------------------------------------- stage 2

@@ -154,6 +154,8 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   a.pool_half = pool_k / 2;
   a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
   a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
+  // workgroups of the score passes (the launcher splits them into row-block classes, each
+  // with its own per-sequence ranges in wg_off); the total must fit one grid
   int64_t wg = 0;
   a.wg_off[0] = 0;
   for (int b = 0; b < batch->batch; ++b) {

@@ -143,6 +143,43 @@ def m_pack_high_nibble_first(q, qfmt, bits):
     return _orig["pack_codes"](q, qfmt, bits)
 
 
+def m_lse_added(q_group, k_rows, scale, lse):
+    R = q_group.shape[0]
+    raw = np.zeros(k_rows.shape[0])
+    for r in range(R):
+        raw += np.exp(scale * (q_group[r] @ k_rows.T) + np.asarray(lse[r])[:, None]).sum(axis=0)  # sign flipped
+    return raw / R
+
+
+def m_lse_base2(q_group, k_rows, scale, lse):
+    R = q_group.shape[0]
+    raw = np.zeros(k_rows.shape[0])
+    for r in range(R):
+        raw += np.exp2(scale * (q_group[r] @ k_rows.T) - np.asarray(lse[r])[:, None]).sum(axis=0)
+    return raw / R
+
+
+def m_lse_first_row_only(q_group, k_rows, scale, lse):
+    lse = np.asarray(lse, dtype=np.float64)
+    return _orig["guide_attention_sum_given_lse"](q_group, k_rows, scale, np.repeat(lse[:, :1], lse.shape[1], axis=1))
+
+
+def m_lognorm_not_causal_self(q_rows, k_rows, scale, kg_rows=None):
+    if kg_rows is None:
+        return _orig["guide_log_normalisers"](q_rows, k_rows, scale)
+    g = q_rows.shape[0]
+    x = scale * (q_rows @ k_rows.T)
+    y = scale * (q_rows @ kg_rows.T)
+    y = np.where(np.arange(g)[None, :] < np.arange(g)[:, None], y, -np.inf)  # own key left out
+    z = np.concatenate([x, y], axis=1)
+    m = z.max(axis=1)
+    return m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+
+
+def m_lognorm_log2(q_rows, k_rows, scale, kg_rows=None):
+    return _orig["guide_log_normalisers"](q_rows, k_rows, scale, kg_rows) / math.log(2.0)
+
+
 # ----------------------------------------------------------------------------- pins to run
 P = pins
 CASES = [
@@ -165,6 +202,12 @@ CASES = [
     ("combine", m_combine_f64, [P.test_combine_mul_is_fp32_product]),
     ("keep_count", m_keep_count_ceil, [P.test_keep_count_golden]),
     ("pack_codes", m_pack_high_nibble_first, [P.test_int4_packing]),
+    ("guide_attention_sum_given_lse", m_lse_added, [P.test_given_lse_with_the_true_normaliser_is_the_softmax]),
+    ("guide_attention_sum_given_lse", m_lse_base2, [P.test_given_lse_with_the_true_normaliser_is_the_softmax]),
+    ("guide_attention_sum_given_lse", m_lse_first_row_only, [P.test_given_lse_shift_scales_each_row]),
+    ("guide_log_normalisers", m_lognorm_not_causal_self, [P.test_log_normalisers_closed_form]),
+    ("guide_log_normalisers", m_lognorm_log2, [P.test_log_normalisers_closed_form,
+                                                P.test_log_normalisers_vs_scipy_logsumexp]),
 ]
 
 

@@ -180,6 +180,60 @@ def test_guide_keys_closed_form_and_mass():
     assert np.all(mass < 1.0) and np.all(mass > 0.0)
 
 
+def test_log_normalisers_closed_form():
+    """All logits equal (Q = 0): row j's normaliser is the count of keys it sees, so its log is
+    ln N over the context, ln(N + j + 1) with the guide keys 0..j."""
+    N, G, d = 37, 6, 8
+    q = np.zeros((G, d))
+    k = rng.standard_normal((N, d))
+    kg = rng.standard_normal((G, d))
+    np.testing.assert_allclose(o.guide_log_normalisers(q, k, 0.3), np.full(G, math.log(N)), rtol=1e-14)
+    np.testing.assert_allclose(o.guide_log_normalisers(q, k, 0.3, kg), np.log(N + np.arange(G) + 1.0), rtol=1e-14)
+
+
+def test_log_normalisers_vs_scipy_logsumexp():
+    """Random rows: the context-only normaliser is scipy's logsumexp of the scaled logits, and
+    with guide keys it is the logsumexp over the context keys plus the visible guide keys."""
+    N, G, d, scale = 300, 5, 32, 0.2
+    q = rng.standard_normal((G, d)) * 3
+    k = rng.standard_normal((N, d)) * 3
+    kg = rng.standard_normal((G, d)) * 3
+    ref = scipy.special.logsumexp(scale * (q @ k.T), axis=1)
+    np.testing.assert_allclose(o.guide_log_normalisers(q, k, scale), ref, rtol=1e-13)
+    ref_kg = [scipy.special.logsumexp(np.concatenate([scale * (k @ q[j]), scale * (kg[:j + 1] @ q[j])]))
+              for j in range(G)]
+    np.testing.assert_allclose(o.guide_log_normalisers(q, k, scale, kg), ref_kg, rtol=1e-13)
+
+
+def test_given_lse_with_the_true_normaliser_is_the_softmax():
+    """G = R = K = 1 and lse = scipy's logsumexp: the score is scipy's softmax; with a guide
+    of G rows each given its own logsumexp, the raw scores sum to G (every row sums to 1)."""
+    N, d, scale = 500, 64, 0.125
+    q = rng.standard_normal(d) * 2
+    k = rng.standard_normal((N, d)) * 2
+    lse = np.array([[scipy.special.logsumexp(scale * (k @ q))]])
+    s = o.key_scores_given_lse(q[None, None, :], k, scale, 1, lse)
+    np.testing.assert_allclose(s, scipy.special.softmax(scale * (k @ q)), rtol=1e-12, atol=1e-300)
+    G = 7
+    qg = rng.standard_normal((2, G, d))
+    lse = scipy.special.logsumexp(scale * (qg @ k.T), axis=2)
+    raw = o.guide_attention_sum_given_lse(qg, k, scale, lse)
+    assert abs(raw.sum() - G) < 1e-10
+
+
+def test_given_lse_shift_scales_each_row():
+    """Raising row j's lse by delta_j divides its weights by exp(delta_j): with one guide row
+    per head the raw score scales by exp(-delta); rows with different deltas mix."""
+    N, G, d, scale = 64, 3, 16, 0.25
+    q = rng.standard_normal((1, G, d))
+    k = rng.standard_normal((N, d))
+    lse = scipy.special.logsumexp(scale * (q @ k.T), axis=2)
+    delta = np.array([[0.5, -1.25, 2.0]])
+    got = o.guide_attention_sum_given_lse(q, k, scale, lse + delta)
+    want = sum(scipy.special.softmax(scale * (k @ q[0, j])) * math.exp(-delta[0, j]) for j in range(G))
+    np.testing.assert_allclose(got, want, rtol=1e-12)
+
+
 def test_guide_keys_reduce_to_context_softmax():
     """Guide keys whose logits lie 1000 below the context's leave A equal to the context-only
     softmax: their weight underflows to exactly 0 in float64."""
