@@ -45,6 +45,7 @@ def algorithmic_bytes(w, kept_total_per_head):
     per = {
         "k_guide_stats": LH * n * 2 * d + q_bytes + rows * nch * 8,     # read K, write chunk stats
         "k_guide_lse": rows * (nch * 8 + 4),                            # merge chunk stats
+        "k_lse_import": rows * 8,                                       # supplied normalisers -> log2
         "k_guide_attn": LH * n * (2 * d + 4) + q_bytes,                 # read K, write raw
         "k_guide_pool": LH * n * (4 + 4),                               # read raw, write s_key
         "k_quantize": LH * n * (2 * d + rb + 4),                        # read V, write codes and scales
@@ -131,6 +132,34 @@ def cpu_baseline(w, seconds: float):
                       f"(numpy float64; BLAS threads = cores)"}
 
 
+def prefill_lse(w, q, k, kg=None):
+    """The guide rows' natural-log normalisers that a prefill attention kernel exports (input
+    preparation for --given-lse, outside the timed region): fp32 logits from torch matmuls,
+    one (layer, KV head) at a time."""
+    import torch
+
+    out = torch.empty(w.L * w.Hq * w.g_tot, dtype=torch.float32, device=q.device)
+    qv = q.view(w.L, w.Hq, w.g_tot, w.d)
+    kv = k.view(w.L, w.Hkv, w.n_tot, w.d)
+    kgv = kg.view(w.L, w.Hkv, w.g_tot, w.d) if kg is not None else None
+    ov = out.view(w.L, w.Hq, w.g_tot)
+    offs, goff = w.ctx_offsets(), w.guide_offsets()
+    for b in range(w.batch):
+        g0, g1, n0, n1 = goff[b], goff[b + 1], offs[b], offs[b + 1]
+        for l in range(w.L):
+            for h in range(w.Hkv):
+                qs = qv[l, h * w.R:(h + 1) * w.R, g0:g1].float().reshape(-1, w.d)
+                x = (qs @ kv[l, h, n0:n1].float().T) * w.softmax_scale
+                if kgv is not None:
+                    y = (qs @ kgv[l, h, g0:g1].float().T) * w.softmax_scale
+                    j = torch.arange(g1 - g0, device=q.device)
+                    y = y.masked_fill((j[None, :] > j[:, None]).repeat(w.R, 1), float("-inf"))
+                    x = torch.cat([x, y], dim=1)
+                ov[l, h * w.R:(h + 1) * w.R, g0:g1] = torch.logsumexp(x, dim=1).view(w.R, g1 - g0)
+    torch.cuda.synchronize()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +170,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--guide-keys", action="store_true",
                     help="paper-literal normaliser: include the appended guide's own keys")
+    ap.add_argument("--given-lse", action="store_true",
+                    help="guide rows' log-normalisers supplied (as a prefill attention kernel exports them): "
+                         "score pass 1 is skipped")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
@@ -156,15 +188,15 @@ def main():
         return
 
     from paper_2608_03276_amd import binding as B
+    from synth import device as SD
     from synth import workloads as W
-
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    import parity_util as pu
 
     w = W.ALL[args.workload]()
     torch.cuda.set_device(0)
-    q, k, v = pu.device_inputs(w)
-    kg = pu.device_guide_keys(w) if args.guide_keys else None
+    q, k, v = SD.device_inputs(w)
+    kg = SD.device_guide_keys(w) if args.guide_keys else None
+    lse = prefill_lse(w, q, k, kg) if args.given_lse else None
+    kg_arg = None if args.given_lse else kg
     d = B.dims(w.L, w.Hq, w.Hkv, w.d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
     ko = B.kept_offsets_for(bt, w.keep_ratio or 0.0, w.keep_budget or 0)
@@ -174,7 +206,7 @@ def main():
     def step(ev=None):
         B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
                    w.keep_budget or 0, ko, bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c,
-                   bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev, k_guide=kg)
+                   bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev, k_guide=kg_arg, guide_lse=lse)
 
     for _ in range(args.warmup):
         step()
@@ -188,7 +220,9 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
-    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(STAGES)}
+    stages = STAGES if lse is None else ["pass1_skipped", "k_lse_import"] + STAGES[2:]
+    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(stages)}
+    stage_ms.pop("pass1_skipped", None)
 
     per, path_bytes = algorithmic_bytes(w, ko[-1])
     # the two score passes are bf16 contractions (2 flop per guide-row x token x dim); the
@@ -227,7 +261,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
-        "config": {"workload": w.describe() + (", guide keys in the normaliser" if kg is not None else ""),
+        "config": {"workload": w.describe() + (", guide keys in the normaliser" if kg is not None else "")
+                   + (", row normalisers supplied by the prefill (score pass 1 skipped)" if lse is not None else ""),
                    "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
                    "context_tokens": w.n_tot, "guide_tokens": w.g_tot, "kept_per_head": ko[-1]},
         "roofline": roofline,
@@ -236,7 +271,7 @@ def main():
         "stages_ms": {n: round(t, 4) for n, t in stage_ms.items()},
         "kernel_rooflines": {n: {k: v for k, v in roofline_of(n).items()
                                  if k in ("bound", "achieved", "unit", "frac", "other_roof")}
-                             for n in STAGES if n != "k_guide_lse"},
+                             for n in stage_ms if n not in ("k_guide_lse", "k_lse_import")},
     }
     del q, k, v, kg, bufs
     if not args.no_cpu_baseline:

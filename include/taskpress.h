@@ -141,6 +141,23 @@ tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void
                           float* s_key, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Step 1 with the row normalisers supplied by the caller.  Sec. 3.2 takes A from the
+ * attention map of the prefill over the context with the guide appended; the prefill
+ * attention kernel already holds, for every guide row, the log-sum-exp of its scaled logits
+ * over the keys it attended to.  Given those, the score needs one pass over K instead of two:
+ *   A^(r)[j][i] = exp(softmax_scale * <q_guide[l][r][g0+j], k[l][h][n0+i]> - guide_lse[l][r][g0+j])
+ * and raw, s_key exactly as for tp_guide_scores.  With guide_lse equal to
+ * ln Z_j of tp_guide_scores (either normaliser) the results agree with it to rounding.
+ * guide_lse: device fp32 [L][Hq][G_tot], natural log, finite, 4-byte aligned; it must
+ * include softmax_scale in the logits (the convention of flash-attention's exported
+ * log-sum-exp).  Other arguments and errors as for tp_guide_scores (same workspace size).
+ */
+tp_status tp_guide_scores_lse(const tp_dims* dims, const tp_batch* batch, const void* q_guide,
+                              const void* k, const float* guide_lse, float softmax_scale,
+                              int32_t pool_k, float* s_key, void* workspace, size_t ws_bytes,
+                              void* stream);
+
+/*
  * Step 2 — value score of Eq. 2 (Sec. 3.3), fused with per-token quantisation of V
  * (KIVI-style per-token scheme cited in Sec. 3.3; int4 cache of Sec. 4 setup):
  *   gamma[l][h][t] = fl32( max_c |v[l][h][t][c]| / qmax )
@@ -198,7 +215,8 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
  * = TP_EVICT_EVENTS, tp_evict records events[i] (hipEvent_t created by the caller) on the
  * stream: [0] before the work, [1] after score pass 1, [2] after the row normalisers,
  * [3] after score pass 2, [4] after pooling, [5] after the V quantisation, [6] after the
- * selection, [7] after the compaction; one kernel runs between consecutive events.
+ * selection, [7] after the compaction; one kernel runs between consecutive events (with
+ * guide_lse, none between [0] and [1], and [1]..[2] converts the supplied normalisers).
  * num_events = 0 (or a NULL profile) records none.
  */
 #define TP_EVICT_EVENTS 8
@@ -212,6 +230,8 @@ typedef struct tp_profile {
  * tp_guide_scores + tp_quantize_v_scales + tp_combine_select_topk + tp_compact_kv
  * (bit-identical outputs; Sec. 3.2-3.4 as for the separate calls), validated as a whole
  * before anything is enqueued, with optional per-kernel timing events.
+ * guide_lse: NULL, or the guide rows' log-normalisers as for tp_guide_scores_lse (then score
+ * pass 1 is skipped); k_guide and guide_lse may not both be given (TP_ERR_PARAM).
  * Outputs: s_key, scales, v_q (required: the compact cache is gathered from it), s_out
  * (optional), kept_idx, k_out, v_q_out, scales_out.
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
@@ -219,7 +239,8 @@ typedef struct tp_profile {
  * Every argument is validated before anything is enqueued.  Errors as for the four calls.
  */
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                   const void* k_guide, const void* v, float softmax_scale, int32_t pool_k,
+                   const void* k_guide, const float* guide_lse, const void* v, float softmax_scale,
+                   int32_t pool_k,
                    int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio, int64_t keep_budget,
                    const int64_t* kept_offsets,
                    float* s_key, float* scales, void* v_q, float* s_out, int32_t* kept_idx,

@@ -22,7 +22,8 @@ TP_MAX_BATCH = 64
 TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
-            "tp_guide_scores", "tp_quantize_v_scales", "tp_combine_select_topk", "tp_compact_kv", "tp_evict")
+            "tp_guide_scores", "tp_guide_scores_lse", "tp_quantize_v_scales", "tp_combine_select_topk",
+            "tp_compact_kv", "tp_evict")
 
 
 class TaskPressError(RuntimeError):
@@ -108,6 +109,8 @@ def load():
     lib.tp_workspace_size.argtypes = [ctypes.c_int32, pd, pb, ctypes.POINTER(ctypes.c_size_t)]
     lib.tp_guide_scores.restype = ctypes.c_int32
     lib.tp_guide_scores.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
+    lib.tp_guide_scores_lse.restype = ctypes.c_int32
+    lib.tp_guide_scores_lse.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
     lib.tp_quantize_v_scales.restype = ctypes.c_int32
     lib.tp_quantize_v_scales.argtypes = [pd, pb, P, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.tp_combine_select_topk.restype = ctypes.c_int32
@@ -116,7 +119,7 @@ def load():
     lib.tp_compact_kv.restype = ctypes.c_int32
     lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
     lib.tp_evict.restype = ctypes.c_int32
-    lib.tp_evict.argtypes = [pd, pb, P, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+    lib.tp_evict.argtypes = [pd, pb, P, P, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                              ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64, P, P, P, P, P, P, P, P, P,
                              ctypes.c_size_t, ctypes.POINTER(TpProfile), P]
     _lib = lib
@@ -186,6 +189,20 @@ def tp_guide_scores(d: TpDims, batch: Batch, q_guide, k, softmax_scale: float, p
                                   float(softmax_scale), int(pool_k), _ptr(s_key), _ptr(workspace),
                                   workspace.numel() * workspace.element_size() if workspace is not None else 0,
                                   _stream(stream)))
+
+
+def tp_guide_scores_lse(d: TpDims, batch: Batch, q_guide, k, guide_lse, softmax_scale: float, pool_k: int, s_key,
+                        workspace, stream=None):
+    """Step 1 with the guide rows' log-normalisers supplied: guide_lse fp32 [L][Hq][G_tot]
+    (natural log of each row's softmax normaliser over the scaled logits)."""
+    L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
+    _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(guide_lse, L * Hq * batch.g_tot * 4, "guide_lse")
+    _need(s_key, L * Hkv * batch.n_tot * 4, "s_key")
+    _check(load().tp_guide_scores_lse(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k),
+                                      _ptr(guide_lse), float(softmax_scale), int(pool_k), _ptr(s_key),
+                                      _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def row_bytes(qfmt: int, bits: int, head_dim: int) -> int:
@@ -280,7 +297,7 @@ def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_
 
 def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
              rule: int, keep_ratio: float, keep_budget: int, kept_offsets, s_key, scales, v_q, s_out, kept_idx,
-             k_out, v_q_out, scales_out, workspace, events=None, stream=None, k_guide=None):
+             k_out, v_q_out, scales_out, workspace, events=None, stream=None, k_guide=None, guide_lse=None):
     """The whole path in one call.  `events`: None, or TP_EVICT_EVENTS torch.cuda.Event objects
     (enable_timing=True) that the library records between its kernels."""
     L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
@@ -289,6 +306,7 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
     _need(k, L * Hkv * n * D * 2, "k")
     _need(v, L * Hkv * n * D * 2, "v")
     _need(k_guide, L * Hkv * batch.g_tot * D * 2, "k_guide")
+    _need(guide_lse, L * Hq * batch.g_tot * 4, "guide_lse")
     for t, nbytes, name in ((s_key, L * Hkv * n * 4, "s_key"), (scales, L * Hkv * n * 4, "scales"),
                             (v_q, L * Hkv * n * row_bytes(qfmt, bits, D), "v_q")):
         _need(t, nbytes, name)
@@ -305,7 +323,8 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
             handles.append(e.cuda_event)
         prof = TpProfile(TP_EVICT_EVENTS, (ctypes.c_void_p * TP_EVICT_EVENTS)(*handles))
     ws = workspace
-    _check(load().tp_evict(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(k_guide), _ptr(v),
+    _check(load().tp_evict(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(k_guide),
+                           _ptr(guide_lse), _ptr(v),
                            float(softmax_scale), int(pool_k), int(qfmt), int(bits), int(rule), float(keep_ratio),
                            int(keep_budget), ko, _ptr(s_key), _ptr(scales), _ptr(v_q), _ptr(s_out),
                            _ptr(kept_idx), _ptr(k_out), _ptr(v_q_out), _ptr(scales_out), _ptr(ws),
@@ -314,12 +333,12 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
 
 def evict_fused(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int,
                 bits: int, rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0,
-                bufs: EvictBuffers = None, events=None, stream=None, k_guide=None) -> EvictBuffers:
+                bufs: EvictBuffers = None, events=None, stream=None, k_guide=None, guide_lse=None) -> EvictBuffers:
     """The whole path through tp_evict; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
     ko = kept_offsets_for(batch, keep_ratio, keep_budget)
     if bufs is None:
         bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
     tp_evict(d, batch, q_guide, k, v, softmax_scale, pool_k, qfmt, bits, rule, keep_ratio, keep_budget, ko,
              bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c, bufs.v_q_c, bufs.scales_c,
-             bufs.ws_evict, events, stream, k_guide)
+             bufs.ws_evict, events, stream, k_guide, guide_lse)
     return bufs

@@ -110,8 +110,8 @@ tp_status check_qfmt(int32_t qfmt, int32_t bits) {
 // enqueueing anything, so the fused entry point can validate every step before launching.
 
 tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                        const void* k_guide, float softmax_scale, int32_t pool_k, float* s_key, void* workspace,
-                        size_t ws_bytes, tp::GuideArgs& a) {
+                        const void* k_guide, const float* guide_lse, float softmax_scale, int32_t pool_k,
+                        float* s_key, void* workspace, size_t ws_bytes, tp::GuideArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
   s = check_batch(batch, true);
@@ -119,6 +119,9 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
   if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key) || (k_guide && !aligned16(k_guide)))
     return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (k_guide && guide_lse)
+    return fail(TP_ERR_PARAM, "k_guide and guide_lse are exclusive (supplied normalisers already cover the keys)");
+  if (guide_lse && ((uintptr_t)guide_lse & 3u) != 0) return fail(TP_ERR_PARAM, "guide_lse must be 4-byte aligned");
   if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
     return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
   if (pool_k < 1 || (pool_k & 1) == 0) return fail(TP_ERR_PARAM, "pool_k must be odd and >= 1 (got %d)", pool_k);
@@ -139,6 +142,7 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   a.q = (const uint16_t*)q_guide;
   a.k = (const uint16_t*)k;
   a.kg = (const uint16_t*)k_guide;
+  a.lse_in = guide_lse;
   a.s_key = s_key;
   a.stats = (float2*)((char*)workspace + lay.stats_off);
   a.lse2 = (float*)((char*)workspace + lay.lse_off);
@@ -351,10 +355,23 @@ tp_status tp_guide_scores(const tp_dims* dims, const tp_batch* batch, const void
                           void* workspace, size_t ws_bytes, void* stream) {
   tp::GuideArgs a;
   const tp_status s =
-      prepare_guide(dims, batch, q_guide, k, k_guide, softmax_scale, pool_k, s_key, workspace, ws_bytes, a);
+      prepare_guide(dims, batch, q_guide, k, k_guide, nullptr, softmax_scale, pool_k, s_key, workspace, ws_bytes, a);
   if (s != TP_OK) return s;
   const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream, nullptr);
   if (e != hipSuccess) return hip_fail(e, "tp_guide_scores launch");
+  return ok();
+}
+
+tp_status tp_guide_scores_lse(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                              const float* guide_lse, float softmax_scale, int32_t pool_k, float* s_key,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  if (!guide_lse) return fail(TP_ERR_NULL, "guide_lse must be non-NULL");
+  tp::GuideArgs a;
+  const tp_status s = prepare_guide(dims, batch, q_guide, k, nullptr, guide_lse, softmax_scale, pool_k, s_key,
+                                    workspace, ws_bytes, a);
+  if (s != TP_OK) return s;
+  const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "tp_guide_scores_lse launch");
   return ok();
 }
 
@@ -394,7 +411,7 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
 }
 
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                   const void* k_guide, const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
+                   const void* k_guide, const float* guide_lse, const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
                    int64_t keep_budget, const int64_t* kept_offsets, float* s_key, float* scales, void* v_q,
                    float* s_out, int32_t* kept_idx, void* k_out, void* v_q_out, float* scales_out, void* workspace,
                    size_t ws_bytes, const tp_profile* profile, void* stream) {
@@ -413,7 +430,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   const size_t gws = guide_workspace_bytes(dims, batch);
   if (!workspace || ws_bytes < gws) return fail(TP_ERR_WORKSPACE, "workspace needs at least %zu bytes", gws);
   tp::GuideArgs ga;
-  s = prepare_guide(dims, batch, q_guide, k, k_guide, softmax_scale, pool_k, s_key, workspace, gws, ga);
+  s = prepare_guide(dims, batch, q_guide, k, k_guide, guide_lse, softmax_scale, pool_k, s_key, workspace, gws, ga);
   if (s != TP_OK) return s;
   tp::QuantArgs qa;
   s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);

@@ -617,6 +617,12 @@ __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
   }
 }
 
+// Row normalisers supplied by the caller (natural log) -> the log2 domain of pass 2.
+__global__ __launch_bounds__(256) void k_lse_import(const float* lse, float* lse2, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) lse2[i] = (float)((double)lse[i] * 1.4426950408889634);
+}
+
 template <int D, int NP>
 hipError_t launch_pass(const GuideArgs& a, bool attn, hipStream_t stream) {
   const unsigned nwg = (unsigned)a.wg_off[a.bt.batch];
@@ -653,6 +659,16 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
     for (int c = 0; c < 4; ++c) cls[c].wg_off[b + 1] = (int32_t)wg[c];
   }
   for (int pass = 0; pass < 2; ++pass) {  // the large classes first: shorter tail
+    if (pass == 0 && a.lse_in) {  // normalisers given: no pass 1
+      hipError_t e = ev ? hipEventRecord(ev[0], stream) : hipSuccess;
+      if (e != hipSuccess) return e;
+      const int64_t n = (int64_t)a.L * a.Hq * a.g_tot;
+      hipLaunchKernelGGL(k_lse_import, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a.lse_in, a.lse2, n);
+      e = hipGetLastError();
+      if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
+      if (e != hipSuccess) return e;
+      continue;
+    }
     hipError_t e = launch_pass<D, 4>(cls[3], pass == 1, stream);
     if (e == hipSuccess) e = launch_pass<D, 3>(cls[2], pass == 1, stream);
     if (e == hipSuccess) e = launch_pass<D, 2>(cls[1], pass == 1, stream);

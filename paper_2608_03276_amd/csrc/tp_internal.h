@@ -26,6 +26,7 @@ struct GuideArgs {
   const uint16_t* q;  // bf16 [L][Hq][G_tot][d]
   const uint16_t* k;  // bf16 [L][Hkv][N_tot][d]
   const uint16_t* kg; // bf16 [L][Hkv][G_tot][d] guide keys, or nullptr (context-only normaliser)
+  const float* lse_in;// fp32 [L][Hq][G_tot] caller's natural-log row normalisers, or nullptr
   float* s_key;       // fp32 [L][Hkv][N_tot]
   float2* stats;      // [nchunk_max][L*Hq*G_tot]   per-chunk (max, sum) in the log2 domain
   float* lse2;        // [L*Hq*G_tot]               log2-sum-exp2 of the row's normaliser

@@ -16,6 +16,7 @@ import torch
 
 import synth
 from oracle import taskpress_oracle as o
+from synth.device import device_guide_keys, device_inputs, guide_key_stream  # noqa: F401 (re-exported)
 from paper_2608_03276_amd import binding as B
 
 RTOL = 1e-3
@@ -24,33 +25,6 @@ FLOOR = 2.0 ** -100
 
 def log(msg):
     print(msg, flush=True)
-
-
-def device_inputs(w, device="cuda"):
-    """Q/K/V of workload `w` drawn on the GPU (bit-identical to the host generator)."""
-    lens = list(w.ctx_lens)
-    glens = list(w.guide_lens)
-    q = torch.empty(w.L * w.Hq * w.g_tot * w.d, dtype=torch.bfloat16, device=device)
-    k = torch.empty(w.L * w.Hkv * w.n_tot * w.d, dtype=torch.bfloat16, device=device)
-    v = torch.empty_like(k)
-    s = torch.cuda.current_stream().cuda_stream
-    synth.device_fill(q.data_ptr(), w.q, w.L, w.Hq, glens, w.d, s)
-    synth.device_fill(k.data_ptr(), w.k, w.L, w.Hkv, lens, w.d, s)
-    synth.device_fill(v.data_ptr(), w.v, w.L, w.Hkv, lens, w.d, s)
-    return q, k, v
-
-
-def guide_key_stream(w):
-    """The guide tokens' keys of workload w (N(0,1), same seed as its guide queries)."""
-    return synth.Stream(w.q.seed, synth.TAG_KG)
-
-
-def device_guide_keys(w, device="cuda"):
-    """k_guide bf16 [L][Hkv][G_tot][d] of workload w, drawn on the GPU."""
-    kg = torch.empty(w.L * w.Hkv * w.g_tot * w.d, dtype=torch.bfloat16, device=device)
-    synth.device_fill(kg.data_ptr(), guide_key_stream(w), w.L, w.Hkv, list(w.guide_lens), w.d,
-                      torch.cuda.current_stream().cuda_stream)
-    return kg
 
 
 def host_guide_keys(w, b, l, h):
@@ -65,6 +39,27 @@ def host_segment(w, b, l, h):
     k = synth.rows(w.k, b, l, h, n, w.d)
     v = synth.rows(w.v, b, l, h, n, w.d)
     return qg, k, v
+
+
+def oracle_guide_lse(w, guide_keys=False, jitter_seed=None):
+    """fp32 [L][Hq][G_tot] natural-log row normalisers of workload w from the oracle: what a
+    prefill attention kernel exports for the appended guide rows (context keys, plus guide
+    keys 0..j with guide_keys).  jitter_seed: add a seeded per-row offset in [-1, 1], so
+    that a test sees every row's own value used."""
+    out = np.zeros((w.L, w.Hq, w.g_tot))
+    goff = w.guide_offsets()
+    for b in range(w.batch):
+        g = w.guide_lens[b]
+        for l in range(w.L):
+            for h in range(w.Hkv):
+                kr = o.bf16_to_f64(synth.rows(w.k, b, l, h, w.ctx_lens[b], w.d))
+                kg = o.bf16_to_f64(host_guide_keys(w, b, l, h)) if guide_keys else None
+                for r in range(w.R):
+                    qr = o.bf16_to_f64(synth.rows(w.q, b, l, h * w.R + r, g, w.d))
+                    out[l, h * w.R + r, goff[b]:goff[b] + g] = o.guide_log_normalisers(qr, kr, w.softmax_scale, kg)
+    if jitter_seed is not None:
+        out += np.random.default_rng(jitter_seed).uniform(-1.0, 1.0, out.shape)
+    return out.astype(np.float32)
 
 
 def run_gpu(w, q, k, v, rule=None, bufs=None, k_guide=None):

@@ -109,6 +109,25 @@ def test_guide_scores_validation():
 
 
 @no_gpu
+def test_guide_scores_lse_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300], [0, 16, 20])
+    wsb = B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, d, bt)
+
+    def gl(lse=FAKE, scale=0.125, pool=5, ws=FAKE, nbytes=wsb, batch=bt):
+        return lib.tp_guide_scores_lse(ctypes.byref(d), ctypes.byref(batch.c), FAKE, FAKE, lse, scale, pool, FAKE, ws,
+                                       nbytes, None)
+
+    assert gl(lse=None) == B.TP_ERR_NULL
+    assert gl(lse=FAKE + 2) == B.TP_ERR_PARAM
+    assert gl(scale=-1.0) == B.TP_ERR_PARAM
+    assert gl(pool=4) == B.TP_ERR_PARAM
+    assert gl(nbytes=wsb - 1) == B.TP_ERR_WORKSPACE
+    assert gl(batch=B.Batch([0, 100, 300])) == B.TP_ERR_NULL  # guide offsets needed
+    assert lib.tp_last_error().decode() != ""
+
+
+@no_gpu
 def test_quantize_validation():
     d = B.dims(2, 8, 2, 128)
     bt = B.Batch([0, 100])
@@ -159,7 +178,7 @@ def test_compact_validation():
 
 
 def _ev(d, bt, **kw):
-    a = dict(q=FAKE, k=FAKE, kg=None, v=FAKE, scale=0.125, pool=5, qfmt=0, bits=8, rule=0, ratio=0.25, budget=0,
+    a = dict(q=FAKE, k=FAKE, kg=None, lse=None, v=FAKE, scale=0.125, pool=5, qfmt=0, bits=8, rule=0, ratio=0.25, budget=0,
              ko=None, skey=FAKE, sc=FAKE, vq=FAKE, sout=FAKE, idx=FAKE, kout=FAKE, vqout=FAKE, scout=FAKE,
              ws=FAKE, wsb=1 << 40, prof=None)
     a.update(kw)
@@ -167,7 +186,8 @@ def _ev(d, bt, **kw):
         a["ko"] = B.kept_offsets_for(bt, a["ratio"], a["budget"])
     ko = (ctypes.c_int64 * len(a["ko"]))(*a["ko"])
     prof = ctypes.byref(a["prof"]) if a["prof"] is not None else None
-    return lib.tp_evict(ctypes.byref(d), ctypes.byref(bt.c), a["q"], a["k"], a["kg"], a["v"], a["scale"], a["pool"],
+    return lib.tp_evict(ctypes.byref(d), ctypes.byref(bt.c), a["q"], a["k"], a["kg"], a["lse"], a["v"], a["scale"],
+                        a["pool"],
                         a["qfmt"], a["bits"], a["rule"], a["ratio"], a["budget"], ko, a["skey"], a["sc"], a["vq"],
                         a["sout"], a["idx"], a["kout"], a["vqout"], a["scout"], a["ws"], a["wsb"], prof, None)
 
@@ -199,6 +219,8 @@ def test_evict_validation():
         (dict(prof=null_prof), B.TP_ERR_NULL),
         (dict(k=FAKE + 8), B.TP_ERR_PARAM),
         (dict(kg=FAKE + 4), B.TP_ERR_PARAM),
+        (dict(kg=FAKE, lse=FAKE), B.TP_ERR_PARAM),  # exclusive normaliser sources
+        (dict(lse=FAKE + 2), B.TP_ERR_PARAM),
     ]
     for kw, want in cases:
         assert _ev(d, bt, **kw) == want, kw

@@ -252,6 +252,46 @@ def test_guide_scores_with_guide_keys(gpu_lib, case):
     _guide_case(case, True)
 
 
+def _guide_lse_case(case, jitter_seed):
+    name, L, Hq, Hkv, d, lens, glens, dist, pool = case
+    pu.log(f"guide scores with supplied normalisers, case {name}, jitter {jitter_seed}")
+    out_frac, out_scale = (0.02, 30.0) if dist == synth.DIST_STUDENT_T3 else (0.0, 1.0)
+    w = W.Workload(name, L, Hq, Hkv, d, tuple(lens), tuple(glens), synth.Stream(67, synth.TAG_Q),
+                   synth.Stream(67, synth.TAG_K, dist, out_frac, out_scale), synth.Stream(67, synth.TAG_V),
+                   keep_ratio=0.25, pool_k=pool)
+    q, k, _ = pu.device_inputs(w)
+    lse = pu.oracle_guide_lse(w, jitter_seed=jitter_seed)
+    dd = B.dims(L, Hq, Hkv, d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    s_key = torch.empty(L * Hkv * w.n_tot, dtype=torch.float32, device="cuda")
+    ws = torch.empty(B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, dd, bt), dtype=torch.uint8, device="cuda")
+    B.tp_guide_scores_lse(dd, bt, q, k, torch.from_numpy(lse.ravel()).cuda(), w.softmax_scale, pool, s_key, ws)
+    torch.cuda.synchronize()
+    got = s_key.cpu().numpy().reshape(L * Hkv, w.n_tot)
+    offs, goff = w.ctx_offsets(), w.guide_offsets()
+    worst = 0.0
+    for b in range(w.batch):
+        for l in range(L):
+            for h in range(Hkv):
+                qg, kb, _ = pu.host_segment(w, b, l, h)
+                rows = lse[l, h * w.R:(h + 1) * w.R, goff[b]:goff[b + 1]].astype(np.float64)
+                ref = o.key_scores_given_lse(o.bf16_to_f64(qg), o.bf16_to_f64(kb), w.softmax_scale, pool, rows)
+                worst = max(worst, pu.assert_scores_close(got[l * Hkv + h, offs[b]:offs[b + 1]], ref,
+                                                          f"{name} b={b} l={l} h={h}"))
+    pu.log(f"  max rel err {worst:.3g}")
+
+
+LSE_CASES = GUIDE_CASES[:5] + [GUIDE_CASES[-1]]
+
+
+@pytest.mark.parametrize("jitter", [None, 5])
+@pytest.mark.parametrize("case", LSE_CASES, ids=[c[0] for c in LSE_CASES])
+def test_guide_scores_lse_parity(gpu_lib, case, jitter):
+    """Step 1 with the normalisers supplied (as a prefill kernel exports them), exact and
+    shifted per row."""
+    _guide_lse_case(case, jitter)
+
+
 # ----------------------------------------------------------------------------- whole path
 @pytest.mark.parametrize("rule", [0, 3])
 def test_end_to_end_tiny(gpu_lib, rule):
@@ -346,6 +386,30 @@ def test_evict_with_guide_keys_against_oracle(gpu_lib):
     # the guide keys change the scores (the context mass of a row drops below 1)
     plain = pu.run_gpu(w, q, k, v)
     assert not torch.equal(plain.s_key, bufs.s_key)
+
+
+def test_evict_with_supplied_normalisers_against_oracle(gpu_lib):
+    """tp_evict given the guide rows' log-normalisers of the paper-literal map (context plus
+    causal guide keys, as the prefill kernel would export them): same results as the oracle's
+    guide-key path, and as tp_evict computing them itself from the guide keys."""
+    w = W.ragged8().with_(name="ragged-lse", L=2, ctx_lens=(3000, 1, 700), guide_lens=(32, 5, 128),
+                          keep_budget=300)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    q, k, v = pu.device_inputs(w)
+    lse = torch.from_numpy(pu.oracle_guide_lse(w, guide_keys=True).ravel()).cuda()
+    bufs = B.evict_fused(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                         rule=w.rule, keep_budget=w.keep_budget, guide_lse=lse)
+    torch.cuda.synchronize()
+    for b in range(w.batch):
+        for l in range(w.L):
+            for h in (0, w.Hkv - 1):
+                pu.check_segment(w, bufs, b, l, h, guide_keys=True)
+    kg = pu.device_guide_keys(w)
+    own = B.evict_fused(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+                        rule=w.rule, keep_budget=w.keep_budget, k_guide=kg)
+    torch.cuda.synchronize()
+    pu.assert_scores_close(bufs.s_key.cpu().numpy(), own.s_key.cpu().numpy().astype(np.float64), "lse vs k_guide")
 
 
 def test_evict_profile_events(gpu_lib):
