@@ -26,12 +26,14 @@ STAGES = ["k_guide_stats", "k_guide_lse", "k_guide_attn", "k_guide_pool", "k_qua
 KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip"], "k_guide_lse": ["guide_scores.hip"],
                   "k_guide_attn": ["guide_scores.hip"], "k_guide_pool": ["guide_scores.hip"],
                   "k_quantize": ["quantize.hip", "quant_row.h"], "k_select": ["select.hip"],
-                  "k_compact": ["compact.hip"]}
+                  "k_compact": ["compact.hip"], "k_compact_quant": ["compact.hip", "quant_row.h"],
+                  "k_lse_import": ["guide_scores.hip"]}
 
 
-def algorithmic_bytes(w, kept_total_per_head):
+def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
     """Compulsory HBM bytes of each kernel of the step and of the whole path (see the design
-    notes).  A kernel's bytes are what it must move itself; the path counts K once."""
+    notes).  A kernel's bytes are what it must move itself; the path counts K once.  Without
+    full codes step 2 writes the scales only and the compaction re-reads the kept V rows."""
     from paper_2608_03276_amd import binding as B
 
     LH = w.L * w.Hkv
@@ -51,8 +53,12 @@ def algorithmic_bytes(w, kept_total_per_head):
         "k_quantize": LH * n * (2 * d + rb + 4),                        # read V, write codes and scales
         "k_select": LH * (n * (4 + 4 + 4) + kt * 4),                    # read s_key, scales; write S, kept idx
         "k_compact": LH * kt * (2 * (2 * d + rb + 4) + 4),              # read kept rows + idx, write them
+        "k_compact_quant": LH * kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4),  # read kept K, V, idx; write
     }
     path = LH * (n * (2 * d + 2 * d + rb + 4) + kt * (2 * d + rb + 4 + 2 * d + rb + 4 + 4)) + q_bytes
+    if not full_codes:
+        per["k_quantize"] = LH * n * (2 * d + 4)                        # read V, write scales
+        path = LH * (n * (2 * d + 2 * d + 4) + kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4)) + q_bytes
     return per, path
 
 
@@ -173,6 +179,9 @@ def main():
     ap.add_argument("--given-lse", action="store_true",
                     help="guide rows' log-normalisers supplied (as a prefill attention kernel exports them): "
                          "score pass 1 is skipped")
+    ap.add_argument("--no-full-codes", action="store_true",
+                    help="step 2 writes the scales only and the compaction quantises the kept V rows "
+                         "(the codes of evicted rows are never written)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
@@ -205,7 +214,8 @@ def main():
 
     def step(ev=None):
         B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
-                   w.keep_budget or 0, ko, bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c,
+                   w.keep_budget or 0, ko, bufs.s_key, bufs.scales, None if args.no_full_codes else bufs.v_q,
+                   bufs.s_comb, bufs.kept_idx, bufs.k_c,
                    bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev, k_guide=kg_arg, guide_lse=lse)
 
     for _ in range(args.warmup):
@@ -221,10 +231,12 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
     stages = STAGES if lse is None else ["pass1_skipped", "k_lse_import"] + STAGES[2:]
+    if args.no_full_codes:
+        stages = stages[:-1] + ["k_compact_quant"]
     stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
 
-    per, path_bytes = algorithmic_bytes(w, ko[-1])
+    per, path_bytes = algorithmic_bytes(w, ko[-1], not args.no_full_codes)
     # the two score passes are bf16 contractions (2 flop per guide-row x token x dim); the
     # other kernels stream HBM
     score_flops = 2 * w.L * w.Hq * sum(g * n for g, n in zip(w.guide_lens, w.ctx_lens)) * w.d
@@ -262,7 +274,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
         "config": {"workload": w.describe() + (", guide keys in the normaliser" if kg is not None else "")
-                   + (", row normalisers supplied by the prefill (score pass 1 skipped)" if lse is not None else ""),
+                   + (", row normalisers supplied by the prefill (score pass 1 skipped)" if lse is not None else "")
+                   + (", codes written for the kept rows only" if args.no_full_codes else ""),
                    "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
                    "context_tokens": w.n_tot, "guide_tokens": w.g_tot, "kept_per_head": ko[-1]},
         "roofline": roofline,

@@ -211,6 +211,22 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
                         void* v_q_out, float* scales_out, void* stream);
 
 /*
+ * Step 4 fused with step 2 for the kept rows only: the kept V rows are read in bf16 and
+ * quantised (Eq. 2, Sec. 3.3; per-token scale and codes exactly as tp_quantize_v_scales)
+ * while they are gathered, so the codes of evicted rows are never written:
+ *   k_out[l][h][ko_b + t][:]   = k[l][h][n0_b + idx][:]
+ *   v_q_out[l][h][ko_b + t][:] = codes of v[l][h][n0_b + idx][:]
+ *   scales_out[l][h][ko_b + t] = gamma of that row
+ * with idx = kept_idx[l][h][ko_b + t]; results bit-identical to tp_quantize_v_scales followed
+ * by tp_compact_kv.  v bf16 [L][Hkv][N_tot][d]; every output required.  An index outside
+ * [0, N_b) yields a zero row, zero codes and a zero scale.
+ */
+tp_status tp_compact_quantize_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                                 const int32_t* kept_idx, const void* k, const void* v, int32_t qfmt,
+                                 int32_t bits, void* k_out, void* v_q_out, float* scales_out,
+                                 void* stream);
+
+/*
  * Optional timing hooks of tp_evict, for callers that profile the path.  With num_events
  * = TP_EVICT_EVENTS, tp_evict records events[i] (hipEvent_t created by the caller) on the
  * stream: [0] before the work, [1] after score pass 1, [2] after the row normalisers,
@@ -232,8 +248,10 @@ typedef struct tp_profile {
  * before anything is enqueued, with optional per-kernel timing events.
  * guide_lse: NULL, or the guide rows' log-normalisers as for tp_guide_scores_lse (then score
  * pass 1 is skipped); k_guide and guide_lse may not both be given (TP_ERR_PARAM).
- * Outputs: s_key, scales, v_q (required: the compact cache is gathered from it), s_out
- * (optional), kept_idx, k_out, v_q_out, scales_out.
+ * Outputs: s_key, scales, v_q (optional), s_out (optional), kept_idx, k_out, v_q_out,
+ * scales_out.  With v_q == NULL step 2 computes the scales only and the compaction
+ * quantises the kept V rows itself (tp_compact_quantize_kv): the compact cache is the same
+ * and the codes of the evicted rows are never written.
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
  * pass's workspace followed by the selection's).
  * Every argument is validated before anything is enqueued.  Errors as for the four calls.

@@ -23,7 +23,7 @@ TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
             "tp_guide_scores", "tp_guide_scores_lse", "tp_quantize_v_scales", "tp_combine_select_topk",
-            "tp_compact_kv", "tp_evict")
+            "tp_compact_kv", "tp_compact_quantize_kv", "tp_evict")
 
 
 class TaskPressError(RuntimeError):
@@ -118,6 +118,8 @@ def load():
                                            P, P, P, ctypes.c_size_t, P]
     lib.tp_compact_kv.restype = ctypes.c_int32
     lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
+    lib.tp_compact_quantize_kv.restype = ctypes.c_int32
+    lib.tp_compact_quantize_kv.argtypes = [pd, pb, pi64, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
     lib.tp_evict.restype = ctypes.c_int32
     lib.tp_evict.argtypes = [pd, pb, P, P, P, P, P, ctypes.c_float, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                              ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64, P, P, P, P, P, P, P, P, P,
@@ -295,6 +297,22 @@ def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_
     return bufs
 
 
+def tp_compact_quantize_kv(d: TpDims, batch: Batch, kept_offsets, kept_idx, k, v, qfmt: int, bits: int, k_out,
+                           v_q_out, scales_out, stream=None):
+    L, Hkv, D = d.num_layers, d.num_kv_heads, d.head_dim
+    kt = int(kept_offsets[-1])
+    _need(kept_idx, L * Hkv * kt * 4, "kept_idx")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(v, L * Hkv * batch.n_tot * D * 2, "v")
+    _need(k_out, L * Hkv * kt * D * 2, "k_out")
+    _need(v_q_out, L * Hkv * kt * row_bytes(qfmt, bits, D), "v_q_out")
+    _need(scales_out, L * Hkv * kt * 4, "scales_out")
+    ko = _i64_array(kept_offsets)
+    _check(load().tp_compact_quantize_kv(ctypes.byref(d), ctypes.byref(batch.c), ko, _ptr(kept_idx), _ptr(k), _ptr(v),
+                                         int(qfmt), int(bits), _ptr(k_out), _ptr(v_q_out), _ptr(scales_out),
+                                         _stream(stream)))
+
+
 def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_k: int, qfmt: int, bits: int,
              rule: int, keep_ratio: float, keep_budget: int, kept_offsets, s_key, scales, v_q, s_out, kept_idx,
              k_out, v_q_out, scales_out, workspace, events=None, stream=None, k_guide=None, guide_lse=None):
@@ -333,12 +351,15 @@ def tp_evict(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, pool_
 
 def evict_fused(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_k: int, qfmt: int,
                 bits: int, rule: int = TP_COMBINE_MUL, keep_ratio: float = 0.0, keep_budget: int = 0,
-                bufs: EvictBuffers = None, events=None, stream=None, k_guide=None, guide_lse=None) -> EvictBuffers:
-    """The whole path through tp_evict; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...)."""
+                bufs: EvictBuffers = None, events=None, stream=None, k_guide=None, guide_lse=None,
+                full_codes: bool = True) -> EvictBuffers:
+    """The whole path through tp_evict; returns the buffers (kept_idx, k_c, v_q_c, scales_c, ...).
+    full_codes=False: no code tensor for every token (bufs.v_q untouched); the compaction
+    quantises the kept rows."""
     ko = kept_offsets_for(batch, keep_ratio, keep_budget)
     if bufs is None:
         bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
     tp_evict(d, batch, q_guide, k, v, softmax_scale, pool_k, qfmt, bits, rule, keep_ratio, keep_budget, ko,
-             bufs.s_key, bufs.scales, bufs.v_q, bufs.s_comb, bufs.kept_idx, bufs.k_c, bufs.v_q_c, bufs.scales_c,
-             bufs.ws_evict, events, stream, k_guide, guide_lse)
+             bufs.s_key, bufs.scales, bufs.v_q if full_codes else None, bufs.s_comb, bufs.kept_idx, bufs.k_c,
+             bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events, stream, k_guide, guide_lse)
     return bufs

@@ -91,6 +91,9 @@ size_t select_workspace(const tp_dims* d, const tp_batch* bt) {
   return ((n * sizeof(float)) + 255) & ~(size_t)255;
 }
 
+// Largest quantised magnitude (Eq. 2): 2^(b-1) - 1 for b-bit integers, 448 for E4M3.
+float qmax_of(int32_t qfmt, int32_t bits) { return qfmt == TP_QFMT_INT ? (float)((1 << (bits - 1)) - 1) : 448.0f; }
+
 int row_bytes_of(int32_t qfmt, int32_t bits, int32_t d) {
   return (qfmt == TP_QFMT_INT && bits <= 4) ? d / 2 : d;
 }
@@ -190,7 +193,7 @@ tp_status prepare_quant(const tp_dims* dims, const tp_batch* batch, const void* 
   a.rows = (int64_t)dims->num_layers * dims->num_kv_heads * batch->ctx_offsets[batch->batch];
   a.qfmt = qfmt;
   a.bits = bits;
-  a.qmax = qfmt == TP_QFMT_INT ? (float)((1 << (bits - 1)) - 1) : 448.0f;
+  a.qmax = qmax_of(qfmt, bits);
   return TP_OK;
 }
 
@@ -279,7 +282,26 @@ tp_status prepare_compact(const tp_dims* dims, const tp_batch* batch, const int6
   a.n_tot = batch->ctx_offsets[batch->batch];
   a.k_tot = kept_offsets[batch->batch];
   a.row_bytes = row_bytes_of(qfmt, bits, dims->head_dim);
+  a.qfmt = qfmt;
+  a.bits = bits;
+  a.qmax = qmax_of(qfmt, bits);
   a.bt = batch_args(batch, false);
+  return TP_OK;
+}
+
+// Compaction that quantises the kept V rows while gathering them (no full code tensor).
+tp_status prepare_compact_quant(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                                const int32_t* kept_idx, const void* k, const void* v, int32_t qfmt, int32_t bits,
+                                void* k_out, void* v_q_out, float* scales_out, tp::CompactArgs& a) {
+  if (!v || !v_q_out || !scales_out) return fail(TP_ERR_NULL, "v, v_q_out and scales_out must be non-NULL");
+  if (!aligned16(v)) return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  // the plain gather's checks, with the code and scale outputs fed from placeholders
+  const tp_status s = prepare_compact(dims, batch, kept_offsets, kept_idx, k, v_q_out, scales_out, qfmt, bits, k_out,
+                                      v_q_out, scales_out, a);
+  if (s != TP_OK) return s;
+  a.v = (const uint16_t*)v;
+  a.vq = nullptr;
+  a.scales = nullptr;
   return TP_OK;
 }
 
@@ -410,6 +432,18 @@ tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_
   return ok();
 }
 
+tp_status tp_compact_quantize_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
+                                 const int32_t* kept_idx, const void* k, const void* v, int32_t qfmt, int32_t bits,
+                                 void* k_out, void* v_q_out, float* scales_out, void* stream) {
+  tp::CompactArgs a;
+  const tp_status s = prepare_compact_quant(dims, batch, kept_offsets, kept_idx, k, v, qfmt, bits, k_out, v_q_out,
+                                            scales_out, a);
+  if (s != TP_OK) return s;
+  const hipError_t e = tp::launch_compact(a, dims->num_layers * dims->num_kv_heads, dims->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_compact_quantize_kv launch");
+  return ok();
+}
+
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
                    const void* k_guide, const float* guide_lse, const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
                    int64_t keep_budget, const int64_t* kept_offsets, float* s_key, float* scales, void* v_q,
@@ -425,7 +459,6 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   if (s != TP_OK) return s;
   s = check_batch(batch, true);
   if (s != TP_OK) return s;
-  if (!v_q) return fail(TP_ERR_NULL, "v_q must be non-NULL (the compact cache is built from it)");
   // workspace: the score pass's, then (without s_out) the combined scores
   const size_t gws = guide_workspace_bytes(dims, batch);
   if (!workspace || ws_bytes < gws) return fail(TP_ERR_WORKSPACE, "workspace needs at least %zu bytes", gws);
@@ -440,7 +473,12 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
                      (char*)workspace + gws, ws_bytes - gws, sa);
   if (s != TP_OK) return s;
   tp::CompactArgs ca;
-  s = prepare_compact(dims, batch, kept_offsets, kept_idx, k, v_q, scales, qfmt, bits, k_out, v_q_out, scales_out, ca);
+  // without v_q the codes of the evicted rows are never written: the compaction quantises
+  // the kept V rows itself (same codes and scales)
+  if (v_q)
+    s = prepare_compact(dims, batch, kept_offsets, kept_idx, k, v_q, scales, qfmt, bits, k_out, v_q_out, scales_out, ca);
+  else
+    s = prepare_compact_quant(dims, batch, kept_offsets, kept_idx, k, v, qfmt, bits, k_out, v_q_out, scales_out, ca);
   if (s != TP_OK) return s;
 
   const hipStream_t st = (hipStream_t)stream;

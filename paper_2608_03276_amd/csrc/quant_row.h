@@ -1,5 +1,5 @@
-// Per-token V quantisation of Eq. 2 (Sec. 3.3), shared by the standalone quantisation kernel
-// and the score pass that quantises V alongside the keys:
+// Per-token V quantisation of Eq. 2 (Sec. 3.3), shared by the quantisation kernel and the
+// compaction kernel that quantises only the kept rows:
 //   gamma_t = fl32(max_c |v_tc| / qmax)
 //   q_tc    = clamp(RNE(fl32(v_tc / gamma_t)), -qmax, qmax)    (b-bit integers), or the OCP
 //             E4M3 code of fl32(v_tc / gamma_t), RNE, saturating at 448; gamma_t = 0 gives 0.
@@ -94,6 +94,23 @@ __device__ inline void codes_divided(const uint32_t (&w)[4], float gamma, const 
   }
 }
 
+// Magnitude bits of the absmax of the row whose LPT pieces sit in LPT consecutive lanes (all
+// lanes call together): an integer max of the bf16 magnitudes, reduced across the lanes.
+template <int LPT>
+__device__ inline uint32_t row_absmax_bits(const uint32_t (&w)[4]) {
+  uint32_t mx = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) mx = max(mx, max(w[i] & 0x7FFFu, (w[i] >> 16) & 0x7FFFu));
+  return group_max<LPT>(mx);
+}
+
+// gamma alone (no codes).
+template <int LPT>
+__device__ inline float scale_piece(const uint4& x, const QuantFmt& f) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  return __uint_as_float(row_absmax_bits<LPT>(w) << 16) / f.qmax;
+}
+
 // Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
 // LPT consecutive lanes; every lane of the wave must call this together (the absmax is
 // reduced across lanes).  Returns gamma (the same on all LPT lanes of the row) and the
@@ -101,10 +118,7 @@ __device__ inline void codes_divided(const uint32_t (&w)[4], float gamma, const 
 template <int LPT>
 __device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& out) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  uint32_t mx = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) mx = max(mx, max(w[i] & 0x7FFFu, (w[i] >> 16) & 0x7FFFu));
-  mx = group_max<LPT>(mx);
+  const uint32_t mx = row_absmax_bits<LPT>(w);
   const float amax = __uint_as_float(mx << 16);
   const float gamma = amax / f.qmax;
   // exponent field of the absmax (bf16 and fp32 share it); below 2^-100 (zero rows

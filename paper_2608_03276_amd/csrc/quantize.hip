@@ -13,7 +13,8 @@ constexpr int kQuantThreads = 256;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 8;  // rows in flight per lane group
 
-template <int D>
+// CODES = false: the scales only (no code tensor), which needs only the row absmax.
+template <int D, bool CODES>
 __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
   constexpr int LPT = D / 8;                 // lanes per token row
   constexpr int TPB = kQuantThreads / LPT;   // token rows per block per load
@@ -37,11 +38,16 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t row = base + u * TPB + row_in_block;
-      uint2 c;
-      const float gamma = quant_piece<LPT>(x[u], f, c);
-      if (row >= a.rows) continue;
-      if (sub == 0) a.scales[row] = gamma;
-      if (a.vq != nullptr) store_codes<D>(a.vq, row, sub, f, c);
+      if (CODES) {
+        uint2 c;
+        const float gamma = quant_piece<LPT>(x[u], f, c);
+        if (row >= a.rows) continue;
+        if (sub == 0) a.scales[row] = gamma;
+        store_codes<D>(a.vq, row, sub, f, c);
+      } else {
+        const float gamma = scale_piece<LPT>(x[u], f);
+        if (row < a.rows && sub == 0) a.scales[row] = gamma;
+      }
     }
   }
 }
@@ -55,10 +61,15 @@ hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream)
   const int64_t cap = 256 * 32;  // 256 CUs x 32 resident blocks is plenty to saturate HBM
   if (blocks > cap) blocks = cap;
   if (blocks < 1) blocks = 1;
-  if (head_dim == 128)
-    hipLaunchKernelGGL(k_quantize<128>, dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+  const bool codes = a.vq != nullptr;
+  if (head_dim == 128 && codes)
+    hipLaunchKernelGGL((k_quantize<128, true>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((k_quantize<128, false>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+  else if (codes)
+    hipLaunchKernelGGL((k_quantize<64, true>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(k_quantize<64>, dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+    hipLaunchKernelGGL((k_quantize<64, false>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -83,6 +83,7 @@ hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream);
 struct CompactArgs {
   const int32_t* kept; // [L*Hkv][K_tot]
   const uint16_t* k;   // bf16 [L*Hkv][N_tot][d]
+  const uint16_t* v;   // bf16 [L*Hkv][N_tot][d]: quantise the kept V rows while gathering, or nullptr
   const uint8_t* vq;   // [L*Hkv][N_tot][row_bytes] or nullptr
   const float* scales; // [L*Hkv][N_tot] or nullptr
   uint16_t* k_out;     // [L*Hkv][K_tot][d]
@@ -90,7 +91,8 @@ struct CompactArgs {
   float* scales_out;
   int64_t n_tot, k_tot;
   int32_t row_bytes;
-  int32_t pad_;
+  int32_t qfmt, bits;  // format of the codes when v is set
+  float qmax;
   int64_t kept_off[TP_MAX_BATCH + 1];
   BatchArgs bt;
 };

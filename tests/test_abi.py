@@ -128,6 +128,24 @@ def test_guide_scores_lse_validation():
 
 
 @no_gpu
+def test_compact_quantize_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300])
+
+    def cq(ko=(0, 25, 75), v=FAKE, vqo=FAKE, sco=FAKE, fmt=0, bits=8, kout=FAKE):
+        return lib.tp_compact_quantize_kv(ctypes.byref(d), ctypes.byref(bt.c), B._i64_array(ko), FAKE, FAKE, v, fmt,
+                                          bits, kout, vqo, sco, None)
+
+    assert cq(v=None) == B.TP_ERR_NULL
+    assert cq(vqo=None) == B.TP_ERR_NULL
+    assert cq(sco=None) == B.TP_ERR_NULL
+    assert cq(kout=None) == B.TP_ERR_NULL
+    assert cq(v=FAKE + 8) == B.TP_ERR_PARAM
+    assert cq(ko=(0, 101, 150)) == B.TP_ERR_SHAPE
+    assert cq(bits=1) == B.TP_ERR_PARAM
+
+
+@no_gpu
 def test_quantize_validation():
     d = B.dims(2, 8, 2, 128)
     bt = B.Batch([0, 100])
@@ -201,7 +219,8 @@ def test_evict_validation():
     cases = [
         (dict(q=None), B.TP_ERR_NULL),
         (dict(v=None), B.TP_ERR_NULL),
-        (dict(vq=None), B.TP_ERR_NULL),
+        (dict(vq=None, vqout=None), B.TP_ERR_NULL),  # without v_q the kept rows are quantised: v_q_out needed
+        (dict(vq=None, scout=None), B.TP_ERR_NULL),
         (dict(idx=None), B.TP_ERR_NULL),
         (dict(kout=None), B.TP_ERR_NULL),
         (dict(vqout=None), B.TP_ERR_NULL),

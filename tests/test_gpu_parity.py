@@ -130,6 +130,59 @@ def test_compact_parity(gpu_lib, qfmt, bits, d):
                     assert not ko_[s, t].any() and not vo[s, t].any() and so[s, t] == 0
 
 
+@pytest.mark.parametrize("qfmt,bits,d", [(0, 8, 128), (0, 4, 64), (0, 2, 128), (1, 8, 64), (1, 8, 128)])
+def test_compact_quantize_parity(gpu_lib, qfmt, bits, d):
+    """Quantise-while-gathering: the kept rows' codes and scales equal the oracle's
+    quantisation of those rows, bit for bit; out-of-range indices give zero rows."""
+    pu.log(f"compact+quantise qfmt={qfmt} bits={bits} d={d}")
+    rng = np.random.default_rng(43)
+    L, Hkv, lens = 2, 2, [7, 1300, 1]
+    kept = [3, 401, 1]
+    ntot, kt = sum(lens), sum(kept)
+    rb = B.row_bytes(qfmt, bits, d)
+    vb = synth.host_tensor(synth.Stream(23, synth.TAG_V, synth.DIST_STUDENT_T3, 0.02, 50.0), L, Hkv, lens, d)
+    vb = vb.reshape(L * Hkv, ntot, d)
+    vb[0, 8] = 0                                   # all-zero row (kept below)
+    vb[1, 9, :3] = [0x7F7F, 0xFF7F, 0x0001]        # largest finite bf16 and a subnormal
+    kb = rng.integers(0, 2 ** 16, (L * Hkv, ntot, d), dtype=np.uint16)
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    ko = np.concatenate([[0], np.cumsum(kept)])
+    idx = np.zeros((L * Hkv, kt), dtype=np.int32)
+    for sg in range(L * Hkv):
+        for b in range(len(lens)):
+            pick = rng.choice(lens[b], kept[b], replace=False)
+            if b == 1:
+                pick[:2] = [1, 2]                  # rows 8 and 9 of the batch: the special rows
+            idx[sg, ko[b]:ko[b + 1]] = np.sort(pick)
+    idx[1, 5] = -1
+    idx[2, 10] = lens[1]
+    dd = B.dims(L, Hkv, Hkv, d)
+    bt = B.Batch(offs.tolist())
+    k_out = torch.empty(L * Hkv * kt * d, dtype=torch.bfloat16, device="cuda")
+    vq_out = torch.empty(L * Hkv * kt * rb, dtype=torch.uint8, device="cuda")
+    sc_out = torch.empty(L * Hkv * kt, dtype=torch.float32, device="cuda")
+    B.tp_compact_quantize_kv(dd, bt, ko.tolist(), torch.from_numpy(idx).cuda(), _bf16_tensor(kb), _bf16_tensor(vb),
+                             qfmt, bits, k_out, vq_out, sc_out)
+    torch.cuda.synchronize()
+    ko_ = k_out.view(torch.int16).cpu().numpy().view(np.uint16).reshape(L * Hkv, kt, d)
+    vo = vq_out.cpu().numpy().reshape(L * Hkv, kt, rb)
+    so = sc_out.cpu().numpy().reshape(L * Hkv, kt)
+    rows = o.bf16_to_f64(vb.reshape(-1, d))
+    gr = o.value_scales(rows, qfmt, bits).reshape(L * Hkv, ntot)
+    qr = o.pack_codes(o.quantize_values(rows, gr.reshape(-1), qfmt, bits), qfmt, bits).reshape(L * Hkv, ntot, rb)
+    for sg in range(L * Hkv):
+        for b in range(len(lens)):
+            for t in range(ko[b], ko[b + 1]):
+                i = idx[sg, t]
+                if 0 <= i < lens[b]:
+                    src = offs[b] + i
+                    assert np.array_equal(ko_[sg, t], kb[sg, src])
+                    assert np.array_equal(vo[sg, t], qr[sg, src]), (sg, t)
+                    assert so[sg, t].view(np.uint32) == gr[sg, src].view(np.uint32)
+                else:
+                    assert not ko_[sg, t].any() and not vo[sg, t].any() and so[sg, t] == 0
+
+
 # ----------------------------------------------------------------------------- step 3
 def _select_inputs(rng, L, Hkv, lens, tie_levels):
     n = L * Hkv * sum(lens)
@@ -410,6 +463,25 @@ def test_evict_with_supplied_normalisers_against_oracle(gpu_lib):
                         rule=w.rule, keep_budget=w.keep_budget, k_guide=kg)
     torch.cuda.synchronize()
     pu.assert_scores_close(bufs.s_key.cpu().numpy(), own.s_key.cpu().numpy().astype(np.float64), "lse vs k_guide")
+
+
+def test_evict_without_full_codes(gpu_lib):
+    """tp_evict with v_q = NULL (the kept rows are quantised during the compaction): the
+    compact cache, kept set and scores are bit-identical to the run that writes every code."""
+    for w in (W.tiny().with_(name="tiny-int4", bits=4),
+              W.ragged8().with_(name="ragged-fp8-nocodes", L=2, ctx_lens=(9000, 1, 8193), guide_lens=(32, 128, 7),
+                                keep_budget=500, qfmt=1)):
+        pu.log(f"tp_evict without the full code tensor: {w.describe()}")
+        d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+        bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+        q, k, v = pu.device_inputs(w)
+        kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=w.rule,
+                  keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
+        full = B.evict_fused(d, bt, q, k, v, **kw)
+        lean = B.evict_fused(d, bt, q, k, v, full_codes=False, **kw)
+        torch.cuda.synchronize()
+        for n in ("s_key", "scales", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c"):
+            assert torch.equal(getattr(full, n).view(torch.uint8), getattr(lean, n).view(torch.uint8)), (w.name, n)
 
 
 def test_evict_profile_events(gpu_lib):
