@@ -138,6 +138,66 @@ def cpu_baseline(w, seconds: float):
                       f"(numpy float64; BLAS threads = cores)"}
 
 
+def machine_rates():
+    """Ceilings measured on this machine (microbenchmarks in libtprates.so): best streaming copy
+    and read bandwidth over a few grid sizes, bf16 MFMA, v_exp_f32 and fp32 fma rates, and the
+    shader clock while the MFMA loop runs.  Prints one JSON line."""
+    import ctypes
+
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_03276_amd", "lib", "libtprates.so"))
+    P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.mb_copy.argtypes = [P, P, I64, I32, P]
+    lib.mb_read.argtypes = [P, I64, P, I32, P]
+    lib.mb_exp.argtypes = [P, I32, I32, P]
+    lib.mb_fma.argtypes = [P, I32, I32, P]
+    lib.mb_mfma.argtypes = [P, P, I32, I32, P]
+    torch.cuda.set_device(0)
+    st = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(st.cuda_stream)
+
+    def timed(fn, reps):
+        for _ in range(2):
+            assert fn() == 0
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        for _ in range(reps):
+            assert fn() == 0
+        b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    nbytes = 4 << 30
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    n16 = nbytes // 16
+    copy = {g: 2 * nbytes / timed(lambda g=g: lib.mb_copy(src.data_ptr(), dst.data_ptr(), n16, g, sp), 5) / 1e9
+            for g in (1024, 4096, 16384)}
+    read = {g: nbytes / timed(lambda g=g: lib.mb_read(src.data_ptr(), n16, sink.data_ptr(), g, sp), 5) / 1e9
+            for g in (1024, 4096, 16384)}
+    del src, dst
+    blocks, iters = 2048, 4096
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    t_exp = timed(lambda: lib.mb_exp(out.data_ptr(), blocks, iters, sp), 3)
+    t_fma = timed(lambda: lib.mb_fma(out.data_ptr(), blocks, iters, sp), 3)
+    cyc = torch.zeros(blocks * 4 * 2, dtype=torch.int64, device="cuda")
+    m_iters = 256
+    t_mfma = timed(lambda: lib.mb_mfma(out.data_ptr(), cyc.data_ptr(), blocks, m_iters, sp), 3)
+    c = cyc.view(-1, 2).double().cpu()
+    clock = float((c[:, 0] / (c[:, 1] * 10.0)).median())  # s_memrealtime ticks at 100 MHz
+    res = {
+        "copy_GBps": {str(g): round(v, 1) for g, v in copy.items()},
+        "read_GBps": {str(g): round(v, 1) for g, v in read.items()},
+        "exp2_Tps": round(blocks * 256 * iters * 8 / t_exp / 1e12, 2),
+        "fma_f32_TFLOPs": round(2 * blocks * 256 * iters * 8 / t_fma / 1e12, 1),
+        "mfma_bf16_TFLOPs": round(blocks * 4 * m_iters * 4 * 32768 / t_mfma / 1e12, 1),
+        "shader_clock_GHz_during_mfma": round(clock, 3),
+    }
+    print(json.dumps({"rates": res}), flush=True)
+
+
 def prefill_lse(w, q, k, kg=None):
     """The guide rows' natural-log normalisers that a prefill attention kernel exports (input
     preparation for --given-lse, outside the timed region): fp32 logits from torch matmuls,
@@ -182,6 +242,8 @@ def main():
     ap.add_argument("--no-full-codes", action="store_true",
                     help="step 2 writes the scales only and the compaction quantises the kept V rows "
                          "(the codes of evicted rows are never written)")
+    ap.add_argument("--rates", action="store_true",
+                    help="only run the machine-ceiling microbenchmarks and print them")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
@@ -194,6 +256,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.rates:
+        machine_rates()
         return
 
     from paper_2608_03276_amd import binding as B

@@ -2,6 +2,7 @@
 
 libtaskpress.so   the eviction path (HIP kernels + C ABI), from csrc/
 libtpsynth_*.so   the seeded input generator (host build with gcc, device build with hipcc)
+libtprates.so     microbenchmarks of the machine's ceilings (bench.py --rates), not the path
 """
 from __future__ import annotations
 
@@ -60,6 +61,14 @@ def build_taskpress(verbose: bool = False) -> str:
     return lib
 
 
+def build_rates() -> str:
+    os.makedirs(LIBDIR, exist_ok=True)
+    lib = os.path.join(LIBDIR, "libtprates.so")
+    _run([HIPCC, *HIP_FLAGS, "-shared", "-x", "hip", os.path.join(CSRC, "microbench.hip"), "-o", lib + ".tmp"])
+    os.replace(lib + ".tmp", lib)
+    return lib
+
+
 def build_synth() -> list[str]:
     host = os.path.join(SYNTH, "libtpsynth_host.so")
     dev = os.path.join(SYNTH, "libtpsynth_dev.so")
@@ -74,10 +83,11 @@ def build_synth() -> list[str]:
 
 
 def build_all(verbose: bool = False) -> list[str]:
-    with cf.ThreadPoolExecutor(max_workers=2) as ex:
+    with cf.ThreadPoolExecutor(max_workers=3) as ex:
         f1 = ex.submit(build_taskpress, verbose)
         f2 = ex.submit(build_synth)
-        return [f1.result(), *f2.result()]
+        f3 = ex.submit(build_rates)
+        return [f1.result(), *f2.result(), f3.result()]
 
 
 if __name__ == "__main__":
