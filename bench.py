@@ -22,7 +22,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 
 # The kernels of one tp_evict call, in launch order (the library records an event after each).
-STAGES = ["k_guide_stats", "k_guide_lse", "k_guide_attn", "k_guide_pool", "k_quantize", "k_select", "k_compact"]
+STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_guide_pool", "k_select", "k_compact"]
 KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip"], "k_guide_lse": ["guide_scores.hip"],
                   "k_guide_attn": ["guide_scores.hip"], "k_guide_pool": ["guide_scores.hip"],
                   "k_quantize": ["quantize.hip", "quant_row.h"], "k_select": ["select.hip"],

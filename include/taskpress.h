@@ -229,10 +229,11 @@ tp_status tp_compact_quantize_kv(const tp_dims* dims, const tp_batch* batch, con
 /*
  * Optional timing hooks of tp_evict, for callers that profile the path.  With num_events
  * = TP_EVICT_EVENTS, tp_evict records events[i] (hipEvent_t created by the caller) on the
- * stream: [0] before the work, [1] after score pass 1, [2] after the row normalisers,
- * [3] after score pass 2, [4] after pooling, [5] after the V quantisation, [6] after the
- * selection, [7] after the compaction; one kernel runs between consecutive events (with
- * guide_lse, none between [0] and [1], and [1]..[2] converts the supplied normalisers).
+ * stream, in launch order: [0] before the work, [1] after score pass 1, [2] after the row
+ * normalisers, [3] after the V quantisation, [4] after score pass 2, [5] after pooling,
+ * [6] after the selection, [7] after the compaction; one kernel runs between consecutive
+ * events (with guide_lse, none between [0] and [1], and [1]..[2] converts the supplied
+ * normalisers).
  * num_events = 0 (or a NULL profile) records none.
  */
 #define TP_EVICT_EVENTS 8

@@ -485,9 +485,24 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   hipEvent_t* ev = (profile && profile->num_events) ? (hipEvent_t*)profile->events : nullptr;
   hipError_t e = hipSuccess;
   if (ev) e = hipEventRecord(ev[0], st);
-  if (e == hipSuccess) e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? ev + 1 : nullptr);
-  if (e == hipSuccess) e = tp::launch_quantize(qa, dims->head_dim, st);
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[5], st);
+  // the V quantisation runs between the normalisers and score pass 2: it needs neither, and
+  // pass 2 then starts after a memory-bound kernel instead of right after pass 1, at a
+  // higher power-limited clock
+  struct Mid {
+    const tp::QuantArgs* qa;
+    int head_dim;
+    hipStream_t st;
+    hipEvent_t done;
+  } mid{&qa, dims->head_dim, st, ev ? ev[3] : nullptr};
+  auto quant_between = [](void* c) -> hipError_t {
+    const Mid* m = (const Mid*)c;
+    hipError_t r = tp::launch_quantize(*m->qa, m->head_dim, m->st);
+    if (r == hipSuccess && m->done) r = hipEventRecord(m->done, m->st);
+    return r;
+  };
+  hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr, ev ? ev[5] : nullptr};
+  if (e == hipSuccess)
+    e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, quant_between, &mid);
   if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
   if (e == hipSuccess) e = tp::launch_compact(ca, dims->num_layers * dims->num_kv_heads, dims->head_dim, st);

@@ -638,7 +638,7 @@ hipError_t launch_pass(const GuideArgs& a, bool attn, hipStream_t stream) {
 // (NP = ceil(min(R G_b, 256) / 64)), so short guides do not pay for 256 rows; each class's
 // arguments give the other sequences empty workgroup ranges.
 template <int D>
-hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
+hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, GuideBetween between, void* ctx) {
   static_assert(Cfg<D>::kSubPerWave >= 1, "chunk too small");
   int64_t max_nb = 0, max_gb = 0;
   GuideArgs cls[4];
@@ -666,6 +666,7 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
       hipLaunchKernelGGL(k_lse_import, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a.lse_in, a.lse2, n);
       e = hipGetLastError();
       if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
+      if (e == hipSuccess && between) e = between(ctx);
       if (e != hipSuccess) return e;
       continue;
     }
@@ -680,6 +681,7 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev) {
       hipLaunchKernelGGL(k_guide_lse<D>, lgrid, dim3(256), 0, stream, a);
       e = hipGetLastError();
       if (e == hipSuccess && ev) e = hipEventRecord(ev[1], stream);
+      if (e == hipSuccess && between) e = between(ctx);
       if (e != hipSuccess) return e;
     }
   }
@@ -712,9 +714,10 @@ GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const 
   return w;
 }
 
-hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev) {
-  if (head_dim == 128) return launch_d<128>(a, stream, ev);
-  return launch_d<64>(a, stream, ev);
+hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev,
+                               GuideBetween between, void* ctx) {
+  if (head_dim == 128) return launch_d<128>(a, stream, ev, between, ctx);
+  return launch_d<64>(a, stream, ev, between, ctx);
 }
 
 }  // namespace tp

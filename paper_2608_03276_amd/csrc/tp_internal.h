@@ -51,7 +51,11 @@ GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const 
                                       const int64_t* g_off, int32_t batch);
 
 // ev (optional): 4 events recorded after the stats, lse, attention and pooling kernels.
-hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev);
+// between (optional): called with ctx once the row normalisers are enqueued and before
+// pass 2, to put independent work on the stream there.
+typedef hipError_t (*GuideBetween)(void* ctx);
+hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev,
+                               GuideBetween between = nullptr, void* ctx = nullptr);
 
 // ---------------------------------------------------------------- step 2 (V scales)
 struct QuantArgs {
