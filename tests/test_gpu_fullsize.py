@@ -57,3 +57,34 @@ def test_fullsize_sampled(gpu_lib, name):
         pu.log(f"    {diag}")
     del q, k, v, bufs
     torch.cuda.empty_cache()
+
+
+def test_fullsize_lean_modes(gpu_lib):
+    """The bench's 128K shape in the two other modes of tp_evict: without the code tensor of
+    every token the compact cache is bit-identical, and with the normalisers supplied (fp32
+    logsumexp from torch matmuls, standing in for what the prefill exports) sampled segments
+    match the oracle."""
+    import bench
+
+    w = W.llama8b_128k()
+    pu.log(f"full size, lean modes: {w.describe()}")
+    torch.cuda.empty_cache()
+    q, k, v = pu.device_inputs(w)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=w.rule,
+              keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
+    full = B.evict_fused(d, bt, q, k, v, **kw)
+    lean = B.evict_fused(d, bt, q, k, v, full_codes=False, **kw)
+    torch.cuda.synchronize()
+    for n in ("kept_idx", "k_c", "v_q_c", "scales_c"):
+        assert torch.equal(getattr(full, n).view(torch.uint8), getattr(lean, n).view(torch.uint8)), n
+    del lean
+    lse = bench.prefill_lse(w, q, k)
+    given = B.evict_fused(d, bt, q, k, v, guide_lse=lse, bufs=full, **kw)
+    torch.cuda.synchronize()
+    for (b, l, h) in SAMPLES["llama8b_128k"]:
+        pu.log(f"  oracle segment b={b} l={l} h={h} (normalisers supplied)")
+        pu.log(f"    {pu.check_segment(w, given, b, l, h)}")
+    del q, k, v, full, given, lse
+    torch.cuda.empty_cache()
