@@ -4,8 +4,12 @@
 //
 // One 1024-thread workgroup per segment.  The combined score S is written once (fp32) and
 // ranked through the order-preserving map of its bit pattern to uint32:
-//   - a 4-pass, 8-bit radix select finds the k-th largest key T and how many keys equal to
-//     T are needed (ties go to the lower index);
+//   - a radix select finds the k-th largest key T and how many keys equal to T are needed
+//     (ties go to the lower index): a 12-bit histogram of the top digit while S is formed,
+//     then the keys in T's top-digit bucket are collected into LDS (when they fit; else the
+//     remaining digits re-read S from memory) and their 12-bit and 8-bit digits are ranked
+//     there, so S is read back only twice (collection and compaction) instead of once per
+//     digit;
 //   - an ordered compaction then emits, in ascending token order, every index with key > T
 //     plus the first `need` indices with key == T: its output slot is
 //     #(key > T before i) + min(#(key == T before i), need), from one block-wide scan of a
@@ -20,6 +24,9 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kPerThread = 4;
 constexpr int kBatch = 8;  // keys each thread loads before it touches the histogram
+constexpr int kTopBits = 12;              // first digit: bits 31..20 of the key
+constexpr int kBins = 1 << kTopBits;      // histogram bins (the 8-bit last digit uses 256)
+constexpr int kCandCap = 16384;           // keys of the threshold's top-digit bucket held in LDS
 
 __device__ inline uint32_t order_key(float s) {
   uint32_t b = __float_as_uint(s);
@@ -42,6 +49,35 @@ __device__ inline float combine(int rule, float s, float g, double na, double nb
     }
     default:
       return s * g;
+  }
+}
+
+// Wave 0: the digit of the k-th largest key among the histogram's nbins (highest first) and
+// how many keys of that digit are still needed (krem counts from the top).  Lane l owns the
+// per = nbins/64 digits below nbins - per*l.
+__device__ inline void pick_digit(const uint32_t* hist, int nbins, uint32_t krem, uint32_t* sel) {
+  const int lane = threadIdx.x & 63;
+  const int per = nbins / 64;
+  uint32_t lsum = 0;
+  for (int e = 0; e < per; ++e) lsum += hist[nbins - 1 - per * lane - e];
+  uint32_t incl = lsum;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  const uint32_t excl = incl - lsum;
+  if (excl < krem && krem <= incl) {
+    uint32_t cum = excl;
+    for (int e = 0; e < per; ++e) {
+      const uint32_t c = hist[nbins - 1 - per * lane - e];
+      if (cum + c >= krem) {
+        sel[0] = (uint32_t)(nbins - 1 - per * lane - e);
+        sel[1] = krem - cum;
+        break;
+      }
+      cum += c;
+    }
   }
 }
 
@@ -85,10 +121,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   float* sb = a.s_buf + (int64_t)seg * a.n_tot + n0;
   int32_t* out = a.kept + (int64_t)seg * a.k_tot + a.kept_off[b];
 
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[kBins];
+  __shared__ uint32_t cand[kCandCap];
   __shared__ uint32_t scan_sh[kSelWaves + 1];
   __shared__ double dred[kSelWaves][2];
-  __shared__ uint32_t sel_digit, sel_krem;
+  __shared__ uint32_t sel[2];  // picked digit, keys of it still needed
+  __shared__ uint32_t ncand;
 
   double norm_a = 0.0, norm_b = 0.0;
   if (a.rule == TP_COMBINE_NORM_ADD) {
@@ -117,7 +155,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     norm_b = sqrt(t2);
   }
 
-  for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
+  for (int i = tid; i < kBins; i += kSelThreads) hist[i] = 0;
   __syncthreads();
   // batches of kBatch keys per thread: the loads of a batch are in flight together
   for (int64_t i0 = 0; i0 < nb; i0 += (int64_t)kSelThreads * kBatch) {
@@ -134,18 +172,57 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
       if (i < nb) {
         const float S = combine(a.rule, x[e], y[e], norm_a, norm_b);
         sb[i] = S;
-        atomicAdd(&hist[order_key(S) >> 24], 1u);
+        atomicAdd(&hist[order_key(S) >> (32 - kTopBits)], 1u);
       }
     }
   }
   __syncthreads();
 
-  uint32_t prefix = 0, krem = (uint32_t)k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (pass > 0) {
-      for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
-      __syncthreads();
+  if (wave == 0) pick_digit(hist, kBins, (uint32_t)k, sel);
+  __syncthreads();
+  uint32_t prefix = sel[0], krem = sel[1];
+  const uint32_t bucket = hist[prefix];  // keys sharing T's top digit
+  const bool in_lds = bucket <= (uint32_t)kCandCap;
+  if (tid == 0) ncand = 0;
+  __syncthreads();
+  if (in_lds) {  // collect that bucket's keys (their order does not matter: only counts are used)
+    for (int64_t i0 = 0; i0 < nb; i0 += (int64_t)kSelThreads * kBatch) {
+      float x[kBatch];
+#pragma unroll
+      for (int e = 0; e < kBatch; ++e) {
+        const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+        x[e] = i < nb ? sb[i] : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < kBatch; ++e) {
+        const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
+        const uint32_t key = order_key(x[e]);
+        const bool hit = i < nb && (key >> (32 - kTopBits)) == prefix;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(hit);
+        if (m != 0) {  // one LDS atomic per wave
+          uint32_t base = 0;
+          if (lane == 0) base = atomicAdd(&ncand, (uint32_t)__builtin_popcountll(m));
+          base = __shfl(base, 0);
+          const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          if (hit && base + rank < (uint32_t)kCandCap) cand[base + rank] = key;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // the two remaining digits: bits 19..8 (12 bits), then bits 7..0 (8 bits)
+  for (int pass = 0; pass < 2; ++pass) {
+    const int shift = pass == 0 ? 8 : 0;
+    const int nbins = pass == 0 ? kBins : 256;
+    const uint32_t mask = (uint32_t)nbins - 1u;
+    for (int i = tid; i < nbins; i += kSelThreads) hist[i] = 0;
+    __syncthreads();
+    if (in_lds) {
+      for (uint32_t i = tid; i < bucket; i += kSelThreads) {
+        const uint32_t key = cand[i];
+        if ((key >> (shift + (pass == 0 ? 12 : 8))) == prefix) atomicAdd(&hist[(key >> shift) & mask], 1u);
+      }
+    } else {
       for (int64_t i0 = 0; i0 < nb; i0 += (int64_t)kSelThreads * kBatch) {
         float x[kBatch];
 #pragma unroll
@@ -157,41 +234,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
         for (int e = 0; e < kBatch; ++e) {
           const int64_t i = i0 + (int64_t)e * kSelThreads + tid;
           const uint32_t key = order_key(x[e]);
-          if (i < nb && (key >> (shift + 8)) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-        }
-      }
-      __syncthreads();
-    }
-    if (wave == 0) {
-      // lane l owns digits 255-4l .. 252-4l, highest first
-      uint32_t c[4], lsum = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        c[e] = hist[255 - 4 * lane - e];
-        lsum += c[e];
-      }
-      uint32_t incl = lsum;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(incl, off);
-        if (lane >= off) incl += y;
-      }
-      const uint32_t excl = incl - lsum;
-      if (excl < krem && krem <= incl) {
-        uint32_t cum = excl;
-        for (int e = 0; e < 4; ++e) {
-          if (cum + c[e] >= krem) {
-            sel_digit = 255u - 4u * lane - e;
-            sel_krem = krem - cum;
-            break;
-          }
-          cum += c[e];
+          if (i < nb && (key >> (shift + (pass == 0 ? 12 : 8))) == prefix) atomicAdd(&hist[(key >> shift) & mask], 1u);
         }
       }
     }
     __syncthreads();
-    prefix = (prefix << 8) | sel_digit;
-    krem = sel_krem;
+    if (wave == 0) pick_digit(hist, nbins, krem, sel);
+    __syncthreads();
+    prefix = (prefix << (pass == 0 ? 12 : 8)) | sel[0];
+    krem = sel[1];
     __syncthreads();
   }
   const uint32_t T = prefix, need = krem;

@@ -247,6 +247,26 @@ def test_select_all_equal_and_zero(gpu_lib):
         assert np.array_equal(kept.cpu().numpy(), np.arange(ko[-1]))
 
 
+def test_select_large_threshold_bucket(gpu_lib):
+    """Keys of the threshold's top digit too many for the LDS candidate buffer (> 16384): the
+    remaining digits are ranked from memory; also a bucket that just fits."""
+    rng = np.random.default_rng(53)
+    for n, levels in [(70000, 2), (40000, 3), (200000, 7)]:
+        sk = (rng.integers(1, levels + 1, n).astype(np.float32) * np.float32(0.25)).astype(np.float32)
+        sk[rng.integers(0, n, 50)] += np.float32(1e-3)   # a few distinct keys inside the buckets
+        g = np.ones(n, np.float32)
+        dd = B.dims(1, 1, 1, 64)
+        bt = B.Batch([0, n])
+        for ratio in (0.3, 0.61, 1.0):
+            ko = B.kept_offsets_for(bt, ratio, 0)
+            kept = torch.empty(ko[-1], dtype=torch.int32, device="cuda")
+            B.tp_combine_select_topk(dd, bt, torch.from_numpy(sk).cuda(), torch.from_numpy(g).cuda(), 0, ratio, 0, ko,
+                                     kept, torch.empty(n, dtype=torch.float32, device="cuda"))
+            torch.cuda.synchronize()
+            S = o.combine(sk, g, 0)
+            assert np.array_equal(kept.cpu().numpy(), o.select(S, ko[-1])), (n, levels, ratio)
+
+
 # ----------------------------------------------------------------------------- step 1
 GUIDE_CASES = [
     # (name, L, Hq, Hkv, d, lens, glens, k-dist, pool)
