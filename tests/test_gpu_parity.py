@@ -87,6 +87,52 @@ def test_quantize_every_bf16_absmax(gpu_lib, qfmt, bits):
     assert len(bad) == 0, f"{len(bad)} rows differ, first absmax bits {hex(int(amax[bad[0]]))}"
 
 
+_EX_AMAX = np.arange(1, 0x7F80, dtype=np.int32)           # every positive finite bf16
+_EX_PER = (_EX_AMAX + 1 + 126) // 127                      # rows per absmax and sign
+_EX_END = np.cumsum(_EX_PER)                               # end row of each absmax (one sign)
+_EX_ROWS = int(_EX_END[-1]) * 2
+
+
+def _exhaustive_block(r0, r1):
+    """Rows r0 .. r1-1 of the exhaustive table [A, v_1 .. v_127]: every (bf16 absmax A, bf16
+    magnitude v <= A) pair once with each sign.  Row r of A (one sign) holds magnitudes
+    127 r .. 127 r + 126, clipped to A (padding zeros); the second half repeats the table
+    with the v's negated."""
+    half = _EX_ROWS // 2
+    idx = np.arange(r0, r1, dtype=np.int64)
+    neg = idx >= half
+    idx = np.where(neg, idx - half, idx)
+    ai = np.searchsorted(_EX_END, idx, side="right")
+    a = _EX_AMAX[ai]
+    r_in_a = idx - (_EX_END[ai] - _EX_PER[ai])
+    v = (r_in_a[:, None] * 127 + np.arange(127, dtype=np.int64)[None, :]).astype(np.int32)
+    v = np.where(v <= a[:, None], v, 0).astype(np.uint16)
+    v[neg] |= np.uint16(0x8000)
+    return np.concatenate([a[:, None].astype(np.uint16), v], axis=1)
+
+
+def test_quantize_every_pair_int8(gpu_lib):
+    """Every (absmax, |v| <= absmax) pair of bf16 values, both signs, int8 (qmax 127): codes and
+    scales bit-exact against the oracle's definition (about 1.07e9 values)."""
+    pu.log(f"quantize every (absmax, v) pair: {_EX_ROWS} rows of 128")
+    group = 1 << 20
+    for g0 in range(0, _EX_ROWS, group):
+        rows = _exhaustive_block(g0, min(_EX_ROWS, g0 + group))
+        n = rows.shape[0]
+        g, q = _run_quant(rows, 1, 1, [n], 128, 0, 8)
+        q = q.reshape(n, 128)
+        step = 1 << 16
+        for r0 in range(0, n, step):
+            vals = o.bf16_to_f64(rows[r0:r0 + step])
+            gr = o.value_scales(vals, 0, 8)
+            qr = o.pack_codes(o.quantize_values(vals, gr, 0, 8), 0, 8)
+            assert np.array_equal(g[r0:r0 + step].view(np.uint32), gr.view(np.uint32)), f"scales, rows {g0 + r0}+"
+            bad = np.nonzero(np.any(q[r0:r0 + step] != qr, axis=1))[0]
+            assert len(bad) == 0, (f"{len(bad)} rows differ from row {g0 + r0 + bad[0]} "
+                                   f"(absmax bits {hex(int(rows[r0 + bad[0], 0]))})")
+        pu.log(f"  rows {g0} .. {g0 + n} match")
+
+
 # ----------------------------------------------------------------------------- step 4
 @pytest.mark.parametrize("qfmt,bits,d", [(0, 8, 128), (0, 4, 64), (1, 8, 64)])
 def test_compact_parity(gpu_lib, qfmt, bits, d):
