@@ -111,21 +111,22 @@ def _exhaustive_block(r0, r1):
     return np.concatenate([a[:, None].astype(np.uint16), v], axis=1)
 
 
-def test_quantize_every_pair_int8(gpu_lib):
-    """Every (absmax, |v| <= absmax) pair of bf16 values, both signs, int8 (qmax 127): codes and
-    scales bit-exact against the oracle's definition (about 1.07e9 values)."""
-    pu.log(f"quantize every (absmax, v) pair: {_EX_ROWS} rows of 128")
+@pytest.mark.parametrize("qfmt,bits", [(0, 8), (0, 4), (1, 8)])
+def test_quantize_every_pair(gpu_lib, qfmt, bits):
+    """Every (absmax, |v| <= absmax) pair of bf16 values, both signs (about 1.07e9 values):
+    codes and scales bit-exact against the oracle's definition, for int8, int4 and E4M3."""
+    pu.log(f"quantize every (absmax, v) pair, qfmt={qfmt} bits={bits}: {_EX_ROWS} rows of 128")
     group = 1 << 20
     for g0 in range(0, _EX_ROWS, group):
         rows = _exhaustive_block(g0, min(_EX_ROWS, g0 + group))
         n = rows.shape[0]
-        g, q = _run_quant(rows, 1, 1, [n], 128, 0, 8)
-        q = q.reshape(n, 128)
+        g, q = _run_quant(rows, 1, 1, [n], 128, qfmt, bits)
+        q = q.reshape(n, B.row_bytes(qfmt, bits, 128))
         step = 1 << 16
         for r0 in range(0, n, step):
             vals = o.bf16_to_f64(rows[r0:r0 + step])
-            gr = o.value_scales(vals, 0, 8)
-            qr = o.pack_codes(o.quantize_values(vals, gr, 0, 8), 0, 8)
+            gr = o.value_scales(vals, qfmt, bits)
+            qr = o.pack_codes(o.quantize_values(vals, gr, qfmt, bits), qfmt, bits)
             assert np.array_equal(g[r0:r0 + step].view(np.uint32), gr.view(np.uint32)), f"scales, rows {g0 + r0}+"
             bad = np.nonzero(np.any(q[r0:r0 + step] != qr, axis=1))[0]
             assert len(bad) == 0, (f"{len(bad)} rows differ from row {g0 + r0 + bad[0]} "
