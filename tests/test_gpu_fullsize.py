@@ -12,12 +12,14 @@ import parity_util as pu
 
 pytestmark = pytest.mark.gpu
 
+# (sequence, layer, KV head) segments checked against the oracle: first, middle and last
+# layers, spread over the KV heads (and over the sequences of the ragged batch)
 SAMPLES = {
     "tiny": [(0, 0, 0), (0, 0, 1)],
-    "llama8b_32k": [(0, 0, 0), (0, 31, 7)],
-    "llama8b_128k": [(0, 0, 0), (0, 17, 3)],
-    "ragged8": [(0, 0, 0), (1, 9, 2), (7, 31, 7)],
-    "widegqa_256k": [(0, 47, 5)],
+    "llama8b_32k": [(0, 0, 0), (0, 16, 3), (0, 31, 7)],
+    "llama8b_128k": [(0, 0, 0), (0, 16, 5), (0, 17, 3), (0, 31, 7)],
+    "ragged8": [(0, 0, 0), (1, 9, 2), (3, 16, 5), (6, 31, 1), (7, 31, 7)],
+    "widegqa_256k": [(0, 0, 0), (0, 24, 3), (0, 47, 5)],
 }
 
 
