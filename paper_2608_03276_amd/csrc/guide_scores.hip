@@ -569,7 +569,7 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
 // sequence).  A block stages kPoolTile + 2*half raw values (summed over row groups) in LDS
 // with coalesced loads, then each thread sums its windows from LDS; windows wider than
 // kPoolMaxHalf use the direct loop.
-constexpr int kPoolTile = 1024;
+constexpr int kPoolTile = 2048;
 constexpr int kPoolMaxHalf = 512;
 
 __device__ inline float raw_at(const GuideArgs& a, const float* raw, int nrg, int64_t j) {
@@ -602,9 +602,20 @@ __global__ __launch_bounds__(256) void k_guide_pool(GuideArgs a) {
     }
     return;
   }
-  for (int t = threadIdx.x; t < kPoolTile + 2 * half; t += 256) {
-    const int64_t j = i0 - half + t;
-    buf[t] = (j >= 0 && j < nb) ? raw_at(a, raw, nrg, j) : 0.f;
+  const int nstage = kPoolTile + 2 * half;
+  for (int t0 = 0; t0 < nstage; t0 += 256 * 8) {  // eight loads in flight per thread
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int t = t0 + 256 * e + threadIdx.x;
+      const int64_t j = i0 - half + t;
+      v[e] = (t < nstage && j >= 0 && j < nb) ? raw_at(a, raw, nrg, j) : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int t = t0 + 256 * e + threadIdx.x;
+      if (t < nstage) buf[t] = v[e];
+    }
   }
   __syncthreads();
 #pragma unroll
