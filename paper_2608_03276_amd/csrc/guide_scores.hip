@@ -264,6 +264,27 @@ __device__ inline void stats_update(const f32x16& acc, float c, float& m, float&
   m = mn;
 }
 
+// The unit's terms exp2(x*c - m) against the lane's current maximum m, summed.
+__device__ inline float unit_sum(const f32x16& acc, float c, float m) {
+  float e[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(acc[j], c, -m));
+#pragma unroll
+  for (int i = 4; i < 16; i += 4)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] += __builtin_amdgcn_exp2f(fmaf(acc[i + j], c, -m));
+  return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+// Lazily updated maximum: the pair's terms are summed against the lanes' current maxima
+// and accepted while a unit's sum stays below 2^64, i.e. while no logit exceeds m by more
+// than about 60 (log2 domain); s then holds sum exp2(x*c - m) for an m that is a logit
+// already seen, which is all the normaliser needs.  A larger sum (the first unit of a row,
+// whose m is still the empty value kNoMax, or a new extreme) is discarded and the unit is
+// redone by the exact online update, which raises m.  This drops the per-logit max and the
+// rescaling from the common case.
+constexpr float kLazyLimit = 18446744073709551616.0f;  // 2^64
+
 // One sub-tile of pass 1, software-pipelined over the NP row-block pairs: step p issues the
 // MFMAs of pair p (query fragments qa, qb, fetched during the previous step) while the
 // vector ALU turns the pending pair (pair p-1, or the previous sub-tile's last pair when
@@ -273,6 +294,7 @@ __device__ inline void stats_steps(const char* qs, const Frag (&kf)[Cfg<D>::kSte
                                    Frag (&qb)[Cfg<D>::kSteps], f32x16& p0, f32x16& p1, float (&sm)[2 * NP],
                                    float (&ss)[2 * NP], float c) {
   using C = Cfg<D>;
+  constexpr int NM = 2 * C::kSteps;  // MFMAs per step
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     f32x16 n0, n1;
@@ -281,10 +303,17 @@ __device__ inline void stats_steps(const char* qs, const Frag (&kf)[Cfg<D>::kSte
     read_qfrag<D>(qs, 2 * pn, qa);
     read_qfrag<D>(qs, 2 * pn + 1, qb);
     const int rb = p == 0 ? 2 * NP - 2 : 2 * p - 2;
-    stats_update(p0, c, sm[rb], ss[rb]);
-    stats_update(p1, c, sm[rb + 1], ss[rb + 1]);
-    pin(sm[rb], ss[rb], sm[rb + 1], ss[rb + 1]);
-    step_schedule<0, 0, 0, 2 * C::kSteps, 2 * C::kSteps, 96 / (2 * C::kSteps), 34 / (2 * C::kSteps) + 1>();
+    const float t0 = unit_sum(p0, c, sm[rb]), t1 = unit_sum(p1, c, sm[rb + 1]);
+    const bool big0 = !(t0 < kLazyLimit), big1 = !(t1 < kLazyLimit);
+    ss[rb] += big0 ? 0.f : t0;
+    ss[rb + 1] += big1 ? 0.f : t1;
+    pin(ss[rb], ss[rb + 1], t0, t1);
+    // 2 x (16 fma + 15 add) + compares, selects and adds; 32 exp2
+    step_schedule<0, 0, 0, NM, NM, (68 + NM - 1) / NM, 32 / NM>();
+    if (__builtin_amdgcn_ballot_w64(big0 || big1)) {  // rare: exact update of those units
+      if (big0) stats_update(p0, c, sm[rb], ss[rb]);
+      if (big1) stats_update(p1, c, sm[rb + 1], ss[rb + 1]);
+    }
     p0 = n0;
     p1 = n1;
   }

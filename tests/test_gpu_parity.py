@@ -329,13 +329,18 @@ GUIDE_CASES = [
     ("wide-pool-direct", 1, 2, 1, 64, [3000], [4], synth.DIST_NORMAL, 1027),
     # one launch per row-block class: 64, 128, 192 and 320 (= 256 + 64) guide rows
     ("row-classes", 2, 8, 2, 128, [9000, 1500, 20000, 4097], [16, 32, 48, 80], synth.DIST_NORMAL, 5),
+    # rare keys scaled x100: their logits jump far above every row's running maximum in the
+    # middle of a chunk, so pass 1 takes its exact re-update of the unit there
+    ("extreme-outliers", 1, 8, 2, 128, [12000, 3000], [64, 16], synth.DIST_NORMAL, 5),
 ]
+# (fraction, scale) of outlier key rows per case
+GUIDE_OUTLIERS = {"heavy-tail-outliers": (0.02, 30.0), "extreme-outliers": (0.003, 100.0)}
 
 
 def _guide_case(case, guide_keys):
     name, L, Hq, Hkv, d, lens, glens, dist, pool = case
     pu.log(f"guide scores case {name}{' with guide keys' if guide_keys else ''}")
-    out_frac, out_scale = (0.02, 30.0) if dist == synth.DIST_STUDENT_T3 else (0.0, 1.0)
+    out_frac, out_scale = GUIDE_OUTLIERS.get(name, (0.0, 1.0))
     w = W.Workload(name, L, Hq, Hkv, d, tuple(lens), tuple(glens), synth.Stream(61, synth.TAG_Q),
                    synth.Stream(61, synth.TAG_K, dist, out_frac, out_scale), synth.Stream(61, synth.TAG_V),
                    keep_ratio=0.25, pool_k=pool)
@@ -375,7 +380,7 @@ def test_guide_scores_with_guide_keys(gpu_lib, case):
 def _guide_lse_case(case, jitter_seed):
     name, L, Hq, Hkv, d, lens, glens, dist, pool = case
     pu.log(f"guide scores with supplied normalisers, case {name}, jitter {jitter_seed}")
-    out_frac, out_scale = (0.02, 30.0) if dist == synth.DIST_STUDENT_T3 else (0.0, 1.0)
+    out_frac, out_scale = GUIDE_OUTLIERS.get(name, (0.0, 1.0))
     w = W.Workload(name, L, Hq, Hkv, d, tuple(lens), tuple(glens), synth.Stream(67, synth.TAG_Q),
                    synth.Stream(67, synth.TAG_K, dist, out_frac, out_scale), synth.Stream(67, synth.TAG_V),
                    keep_ratio=0.25, pool_k=pool)
@@ -401,7 +406,7 @@ def _guide_lse_case(case, jitter_seed):
     pu.log(f"  max rel err {worst:.3g}")
 
 
-LSE_CASES = GUIDE_CASES[:5] + [GUIDE_CASES[-1]]
+LSE_CASES = GUIDE_CASES[:5] + [GUIDE_CASES[-2]]
 
 
 @pytest.mark.parametrize("jitter", [None, 5])
