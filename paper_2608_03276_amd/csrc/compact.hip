@@ -73,7 +73,7 @@ __device__ inline int64_t kept_source(const CompactArgs& a, int seg, int64_t r, 
   return (int64_t)seg * a.n_tot + n0 + (ok ? idx : 0);
 }
 
-template <int D>
+template <int D, int K>
 __global__ __launch_bounds__(kCompactThreads) void k_compact_quant(CompactArgs a) {
   constexpr int LPR = D / 8;
   constexpr int RPB = kCompactThreads / LPR;
@@ -81,6 +81,9 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_quant(CompactArgs a
   const int sub = threadIdx.x % LPR;
   const int64_t r0 = (int64_t)blockIdx.x * RPB * kRowsPerLane + threadIdx.x / LPR;
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
+  __shared__ QuantTables tab;
+  build_tables(tab, a.qmax);
+  __syncthreads();
   int64_t src[kRowsPerLane];
   bool ok[kRowsPerLane];
 #pragma unroll
@@ -99,11 +102,11 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_quant(CompactArgs a
   for (int u = 0; u < kRowsPerLane; ++u) {
     const int64_t r = r0 + u * RPB;
     uint2 c;
-    const float gamma = quant_piece<LPR>(vv[u], f, c);  // every lane of the wave takes part
+    const float gamma = quant_piece<LPR, K>(vv[u], tab, f, c);  // every lane of the wave takes part
     if (r >= a.k_tot) continue;
     const int64_t dst = (int64_t)seg * a.k_tot + r;
     *((uint4*)(a.k_out + dst * D) + sub) = kv[u];
-    store_codes<D>(a.vq_out, dst, sub, f, c);
+    store_codes<D, K>(a.vq_out, dst, sub, c);
     if (sub == 0) a.scales_out[dst] = gamma;
   }
 }
@@ -116,10 +119,18 @@ hipError_t launch_compact(const CompactArgs& a, int segments, int head_dim, hipS
   const int64_t rpb = (int64_t)(kCompactThreads / lpr) * kRowsPerLane;
   const dim3 grid((unsigned)((a.k_tot + rpb - 1) / rpb), (unsigned)segments);
   if (a.v != nullptr) {
-    if (head_dim == 128)
-      hipLaunchKernelGGL(k_compact_quant<128>, grid, dim3(kCompactThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL(k_compact_quant<64>, grid, dim3(kCompactThreads), 0, stream, a);
+    const int kind = qkind_of(a.qfmt, a.bits);
+#define TP_COMPACT_QUANT(D_, K_) hipLaunchKernelGGL((k_compact_quant<D_, K_>), grid, dim3(kCompactThreads), 0, stream, a)
+    if (head_dim == 128) {
+      if (kind == kQByte) TP_COMPACT_QUANT(128, kQByte);
+      else if (kind == kQNibble) TP_COMPACT_QUANT(128, kQNibble);
+      else TP_COMPACT_QUANT(128, kQE4M3);
+    } else {
+      if (kind == kQByte) TP_COMPACT_QUANT(64, kQByte);
+      else if (kind == kQNibble) TP_COMPACT_QUANT(64, kQNibble);
+      else TP_COMPACT_QUANT(64, kQE4M3);
+    }
+#undef TP_COMPACT_QUANT
     return hipGetLastError();
   }
   if (head_dim == 128)

@@ -6,18 +6,28 @@
 //
 // A token row of d bf16 values is held by LPT = d/8 consecutive lanes, 16 bytes each.  The
 // absmax is an integer max of the bf16 magnitude bits (exact), reduced across those lanes
-// with DPP row operations.  The per-element quotient avoids a full IEEE division: the row is
-// rescaled by 2^-e (e = exponent of its absmax, an exact power-of-two scaling that keeps
-// every product and residual in the normal range), the quotient is v' * y with
-// y = 1/gamma' (one correctly rounded division per token), and one residual step
-// fl(q0 + fma(-q0, gamma', v') * y) corrects it.  An exhaustive check over every
-// (absmax, v) pair of bf16 values, for every supported qmax, shows the resulting integer /
-// E4M3 codes equal those of the correctly rounded quotient; rows whose absmax is below
-// 2^-100 use the IEEE division directly.
+// with DPP row operations.
+//
+// Common path (every row of the wave has an absmax A in [2^-50, 2^114)): with A = m * 2^E,
+// m the bf16 significand, gamma = fl32(m/qmax) * 2^E and y' = fl32(1/fl32(m/qmax)) * 2^-E
+// exactly (power-of-two scalings of normal numbers), both read from a 128-entry table per
+// significand that the workgroup computes with IEEE divisions.  The quotient is
+// q0 = v * y' corrected once, fl(q0 + fma(-q0, gamma, v) * y'), and the integer code is the
+// low bits of that value plus 1.5 * 2^23 (an RNE round to an integer whose two's complement
+// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  Every
+// intermediate that can decide a code is a normal number in this range, and an exhaustive
+// check over every (A, v) pair of bf16 values, both signs, for every qmax of the supported
+// formats, gives the codes of the correctly rounded quotient.
+// Other rows (tiny, zero or huge absmax) take the general path: the row is rescaled by
+// 2^-e (e = exponent of the absmax), the same corrected quotient is formed against
+// gamma' = gamma * 2^-e with one division per row, and the code is rounded and clamped
+// explicitly; rows whose absmax is below 2^-100 use the IEEE division directly.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "taskpress.h"
 
 namespace tp {
 
@@ -26,6 +36,34 @@ struct QuantFmt {
   bool nibbles;  // int with b <= 4: two codes per byte, even element in the low nibble
   float qmax;
 };
+
+// Code formats, fixed per kernel instance: one integer code per byte (b in [5, 8]), two per
+// byte (b <= 4), or E4M3.
+enum QKind { kQByte = 0, kQNibble = 1, kQE4M3 = 2 };
+
+__host__ __device__ inline int qkind_of(int32_t qfmt, int32_t bits) {
+  return qfmt == TP_QFMT_INT ? (bits <= 4 ? kQNibble : kQByte) : kQE4M3;
+}
+
+// gamma and 1/gamma of the significand m = 1 + t/128 of an absmax, for the common path.
+struct QuantTables {
+  float g[128];  // fl32(m / qmax)
+  float y[128];  // fl32(1 / g)
+};
+
+// All threads of the block call this, followed by a barrier before the first quant_piece.
+__device__ inline void build_tables(QuantTables& tab, float qmax) {
+  for (int t = threadIdx.x; t < 128; t += blockDim.x) {
+    const float g = (1.0f + (float)t * 0.0078125f) / qmax;
+    tab.g[t] = g;
+    tab.y[t] = 1.0f / g;
+  }
+}
+
+// Absmax exponent fields (bf16 = fp32 exponent field) of the common path: A in [2^-50, 2^114).
+constexpr int kFastExpLo = 77;
+constexpr int kFastExpHi = 240;
+constexpr float kRoundMagic = 12582912.0f;  // 1.5 * 2^23
 
 // max over the LPT (8 or 16) consecutive lanes of a DPP row segment.
 template <int LPT>
@@ -111,32 +149,56 @@ __device__ inline float scale_piece(const uint4& x, const QuantFmt& f) {
   return __uint_as_float(row_absmax_bits<LPT>(w) << 16) / f.qmax;
 }
 
+// Codes of 8 values on the common path: y = v / gamma corrected as above; an integer code is
+// the low bits of y + 1.5 * 2^23.
+template <int K>
+__device__ inline void codes_fast(const uint32_t (&w)[4], float gamma, float ys, uint32_t (&code)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float v = __uint_as_float(h);
+    const float q0 = v * ys;
+    const float y = fmaf(fmaf(-q0, gamma, v), ys, q0);
+    if (K == kQE4M3)
+      code[i] = e4m3_code(__builtin_copysignf(y, v));
+    else
+      code[i] = __float_as_uint(y + kRoundMagic);
+  }
+}
+
 // Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
 // LPT consecutive lanes; every lane of the wave must call this together (the absmax is
-// reduced across lanes).  Returns gamma (the same on all LPT lanes of the row) and the
-// piece's codes: 8 bytes in out.x, out.y, or 8 nibbles in out.x.
-template <int LPT>
-__device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& out) {
+// reduced across lanes, and the path is chosen per wave).  Returns gamma (the same on all
+// LPT lanes of the row) and the piece's codes: 8 bytes in out.x, out.y, or 8 nibbles in out.x.
+template <int LPT, int K>
+__device__ inline float quant_piece(const uint4& x, const QuantTables& tab, const QuantFmt& f, uint2& out) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   const uint32_t mx = row_absmax_bits<LPT>(w);
-  const float amax = __uint_as_float(mx << 16);
-  const float gamma = amax / f.qmax;
-  // exponent field of the absmax (bf16 and fp32 share it); below 2^-100 (zero rows
-  // included) the division path is taken, for the whole wave when any lane needs it
   const int ef = (int)(mx >> 7);
   uint32_t code[8];
-  if (__builtin_amdgcn_ballot_w64(ef <= 27) == 0) {
-    const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
-    const float gs = gamma * sc;
-    codes_scaled(w, sc, gs, 1.0f / gs, f, code);
-  } else if (ef <= 27) {
-    codes_divided(w, gamma, f, code);
+  float gamma;
+  if (__builtin_amdgcn_ballot_w64(ef < kFastExpLo || ef > kFastExpHi) == 0) {
+    const int t = (int)(mx & 0x7Fu);
+    gamma = __builtin_amdgcn_ldexpf(tab.g[t], ef - 127);
+    codes_fast<K>(w, gamma, __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef), code);
   } else {
-    const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
-    const float gs = gamma * sc;
-    codes_scaled(w, sc, gs, 1.0f / gs, f, code);
+    const float amax = __uint_as_float(mx << 16);
+    gamma = amax / f.qmax;
+    // below 2^-100 (zero rows included) the division path is taken, for the whole wave
+    // when any lane needs it
+    if (__builtin_amdgcn_ballot_w64(ef <= 27) == 0) {
+      const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+      const float gs = gamma * sc;
+      codes_scaled(w, sc, gs, 1.0f / gs, f, code);
+    } else if (ef <= 27) {
+      codes_divided(w, gamma, f, code);
+    } else {
+      const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+      const float gs = gamma * sc;
+      codes_scaled(w, sc, gs, 1.0f / gs, f, code);
+    }
   }
-  if (f.nibbles) {
+  if (K == kQNibble) {
     uint32_t p = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) p |= (code[i] & 0xFu) << (4 * i);
@@ -156,10 +218,10 @@ __device__ inline float quant_piece(const uint4& x, const QuantFmt& f, uint2& ou
 
 // Store the codes of one piece: row `row` of a code tensor with `row_bytes` per row, piece
 // `sub` (D/8 pieces per row).  Nontemporal: the codes are streamed out, not re-read here.
-template <int D>
-__device__ inline void store_codes(uint8_t* vq, int64_t row, int sub, const QuantFmt& f, const uint2& c) {
+template <int D, int K>
+__device__ inline void store_codes(uint8_t* vq, int64_t row, int sub, const uint2& c) {
   typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-  if (f.nibbles) {
+  if (K == kQNibble) {
     __builtin_nontemporal_store(c.x, (uint32_t*)(vq + row * (D / 2)) + sub);
   } else {
     u32x2 t;

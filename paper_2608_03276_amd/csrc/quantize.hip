@@ -13,14 +13,22 @@ constexpr int kQuantThreads = 256;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 8;  // rows in flight per lane group
 
-// CODES = false: the scales only (no code tensor), which needs only the row absmax.
-template <int D, bool CODES>
+// K = one of QKind (codes of that format), or kScalesOnly (no code tensor, which needs only the
+// row absmax).
+constexpr int kScalesOnly = -1;
+
+template <int D, int K>
 __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
   constexpr int LPT = D / 8;                 // lanes per token row
   constexpr int TPB = kQuantThreads / LPT;   // token rows per block per load
   const int sub = threadIdx.x % LPT;         // 16-byte piece within the row
   const int row_in_block = threadIdx.x / LPT;
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
+  __shared__ QuantTables tab;
+  if (K != kScalesOnly) {
+    build_tables(tab, a.qmax);
+    __syncthreads();
+  }
 
   for (int64_t base = (int64_t)blockIdx.x * TPB * kUnroll; base < a.rows;
        base += (int64_t)gridDim.x * TPB * kUnroll) {
@@ -38,17 +46,35 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t row = base + u * TPB + row_in_block;
-      if (CODES) {
+      if (K != kScalesOnly) {
         uint2 c;
-        const float gamma = quant_piece<LPT>(x[u], f, c);
+        const float gamma = quant_piece<LPT, (K < 0 ? 0 : K)>(x[u], tab, f, c);
         if (row >= a.rows) continue;
         if (sub == 0) a.scales[row] = gamma;
-        store_codes<D>(a.vq, row, sub, f, c);
+        store_codes<D, (K < 0 ? 0 : K)>(a.vq, row, sub, c);
       } else {
         const float gamma = scale_piece<LPT>(x[u], f);
         if (row < a.rows && sub == 0) a.scales[row] = gamma;
       }
     }
+  }
+}
+
+template <int D>
+void launch_d(const QuantArgs& a, unsigned blocks, hipStream_t stream) {
+  if (a.vq == nullptr) {
+    hipLaunchKernelGGL((k_quantize<D, kScalesOnly>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
+    return;
+  }
+  switch (qkind_of(a.qfmt, a.bits)) {
+    case kQByte:
+      hipLaunchKernelGGL((k_quantize<D, kQByte>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
+      break;
+    case kQNibble:
+      hipLaunchKernelGGL((k_quantize<D, kQNibble>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((k_quantize<D, kQE4M3>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
   }
 }
 
@@ -61,15 +87,10 @@ hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream)
   const int64_t cap = 256 * 32;  // 256 CUs x 32 resident blocks is plenty to saturate HBM
   if (blocks > cap) blocks = cap;
   if (blocks < 1) blocks = 1;
-  const bool codes = a.vq != nullptr;
-  if (head_dim == 128 && codes)
-    hipLaunchKernelGGL((k_quantize<128, true>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
-  else if (head_dim == 128)
-    hipLaunchKernelGGL((k_quantize<128, false>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
-  else if (codes)
-    hipLaunchKernelGGL((k_quantize<64, true>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+  if (head_dim == 128)
+    launch_d<128>(a, (unsigned)blocks, stream);
   else
-    hipLaunchKernelGGL((k_quantize<64, false>), dim3((unsigned)blocks), dim3(kQuantThreads), 0, stream, a);
+    launch_d<64>(a, (unsigned)blocks, stream);
   return hipGetLastError();
 }
 
