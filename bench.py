@@ -25,7 +25,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_guide_pool", "k_select", "k_compact"]
 KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip"], "k_guide_lse": ["guide_scores.hip"],
                   "k_guide_attn": ["guide_scores.hip"], "k_guide_pool": ["guide_scores.hip"],
-                  "k_quantize": ["quantize.hip", "quant_row.h"], "k_select": ["select.hip"],
+                  "k_quantize": ["quantize.hip", "quant_row.h"], "k_quantize_lean": ["quantize.hip", "quant_row.h"],
+                  "k_select": ["select.hip"],
                   "k_compact": ["compact.hip"], "k_compact_quant": ["compact.hip", "quant_row.h"],
                   "k_lse_import": ["guide_scores.hip"]}
 
@@ -59,6 +60,11 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
     if not full_codes:
         per["k_quantize"] = LH * n * (2 * d + 4)                        # read V, write scales
         path = LH * (n * (2 * d + 2 * d + 4) + kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4)) + q_bytes
+    # tp_evict quantises the first half of the V rows (rounded down to 64 rows) on its second
+    # stream beside score pass 1 (k_quantize_lean); the k_quantize launch timed between the
+    # events does the rest
+    rows = LH * n
+    per["k_quantize"] = per["k_quantize"] * (rows - rows // 2 // 64 * 64) // rows
     return per, path
 
 

@@ -255,6 +255,13 @@ typedef struct tp_profile {
  * and the codes of the evicted rows are never written.
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
  * pass's workspace followed by the selection's).
+ * Step 2 of the first half of the V rows runs on a second stream of the library's,
+ * concurrently with score pass 1 (same arithmetic, so the results are as for the separate
+ * calls).  That stream and two events are created, with default priority, by the first
+ * tp_evict call on a device and kept until the process ends (TP_ERR_HIP if that fails); the
+ * work is forked from and joined back to `stream`, so the call stays stream-ordered and may
+ * be captured into a graph.  Calls on one device enqueue one at a time (a lock held while
+ * enqueueing, not while the work runs).
  * Every argument is validated before anything is enqueued.  Errors as for the four calls.
  */
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "tp_internal.h"
@@ -311,6 +312,51 @@ size_t guide_workspace_bytes(const tp_dims* dims, const tp_batch* batch) {
       .total;
 }
 
+// tp_evict's workspace: the score pass's, then the selection's.
+size_t evict_workspace_bytes(const tp_dims* dims, const tp_batch* batch) {
+  return guide_workspace_bytes(dims, batch) + select_workspace(dims, batch);
+}
+
+// The second stream of tp_evict on one device and the events that fork it from, and join it
+// to, the caller's stream: created by the first tp_evict call on that device and kept until
+// the process ends.  `enqueue` is held while a call enqueues its work, so calls from several
+// threads do not interleave their uses of the events.
+struct AuxStream {
+  std::mutex enqueue;
+  bool ready = false;
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+AuxStream g_aux[kMaxDevices];
+std::mutex g_aux_setup;
+
+tp_status aux_stream_for(hipStream_t st, AuxStream*& out) {
+  int dev = 0;
+  hipError_t e = st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "tp_evict: device of the stream");
+  if (dev < 0 || dev >= kMaxDevices) return fail(TP_ERR_UNSUPPORTED, "tp_evict: device %d", dev);
+  AuxStream& a = g_aux[dev];
+  std::lock_guard<std::mutex> lk(g_aux_setup);
+  if (!a.ready) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    // default priority (the caller's streams' priority is not inherited)
+    if (e == hipSuccess && !a.stream) e = hipStreamCreateWithFlags(&a.stream, hipStreamNonBlocking);
+    if (e == hipSuccess && !a.fork) e = hipEventCreateWithFlags(&a.fork, hipEventDisableTiming);
+    if (e == hipSuccess && !a.join) e = hipEventCreateWithFlags(&a.join, hipEventDisableTiming);
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return hip_fail(e, "tp_evict: second stream");
+    a.ready = true;
+  }
+  out = &a;
+  return TP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -366,7 +412,7 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
   if (fn == TP_FN_EVICT) {
     s = check_batch(batch, true);
     if (s != TP_OK) return s;
-    *bytes = guide_workspace_bytes(dims, batch) + select_workspace(dims, batch);
+    *bytes = evict_workspace_bytes(dims, batch);
     return ok();
   }
   return fail(TP_ERR_PARAM, "unknown function id %d", fn);
@@ -461,7 +507,8 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   if (s != TP_OK) return s;
   // workspace: the score pass's, then (without s_out) the combined scores
   const size_t gws = guide_workspace_bytes(dims, batch);
-  if (!workspace || ws_bytes < gws) return fail(TP_ERR_WORKSPACE, "workspace needs at least %zu bytes", gws);
+  const size_t ews = evict_workspace_bytes(dims, batch);
+  if (!workspace || ws_bytes < ews) return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu)", ews, ws_bytes);
   tp::GuideArgs ga;
   s = prepare_guide(dims, batch, q_guide, k, k_guide, guide_lse, softmax_scale, pool_k, s_key, workspace, gws, ga);
   if (s != TP_OK) return s;
@@ -470,7 +517,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   if (s != TP_OK) return s;
   tp::SelectArgs sa;
   s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx, s_out,
-                     (char*)workspace + gws, ws_bytes - gws, sa);
+                     (char*)workspace + gws, ews - gws, sa);
   if (s != TP_OK) return s;
   tp::CompactArgs ca;
   // without v_q the codes of the evicted rows are never written: the compaction quantises
@@ -483,17 +530,36 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
 
   const hipStream_t st = (hipStream_t)stream;
   hipEvent_t* ev = (profile && profile->num_events) ? (hipEvent_t*)profile->events : nullptr;
+  AuxStream* aux = nullptr;
+  s = aux_stream_for(st, aux);
+  if (s != TP_OK) return s;
+  std::lock_guard<std::mutex> lk(aux->enqueue);
+
+  // Step 2 is split in two halves of the V rows.  The first half is quantised by the lean
+  // kernel on the second stream, resident beside score pass 1 (whose workgroups leave one
+  // wave slot and 48 VGPRs per SIMD free) and using its idle memory bandwidth; the second by
+  // the regular kernel between the normalisers and score pass 2, which then starts after a
+  // memory-bound kernel instead of right after pass 1, at a higher power-limited clock.
+  // Every row is quantised once, by one of the two, with the same arithmetic.
+  const int64_t r1 = qa.rows / 2 / 64 * 64;
+  tp::QuantArgs qa1 = qa, qa2 = qa;
+  qa1.rows = r1;
+  qa2.rows = qa.rows - r1;
+  qa2.v += r1 * dims->head_dim;
+  qa2.scales += r1;
+  if (qa2.vq) qa2.vq += r1 * (int64_t)row_bytes_of(qfmt, bits, dims->head_dim);
   hipError_t e = hipSuccess;
   if (ev) e = hipEventRecord(ev[0], st);
-  // the V quantisation runs between the normalisers and score pass 2: it needs neither, and
-  // pass 2 then starts after a memory-bound kernel instead of right after pass 1, at a
-  // higher power-limited clock
+  if (e == hipSuccess) e = hipEventRecord(aux->fork, st);
+  if (e == hipSuccess) e = hipStreamWaitEvent(aux->stream, aux->fork, 0);
+  if (e == hipSuccess) e = tp::launch_quantize_lean(qa1, dims->head_dim, aux->stream);
+  if (e == hipSuccess) e = hipEventRecord(aux->join, aux->stream);
   struct Mid {
     const tp::QuantArgs* qa;
     int head_dim;
     hipStream_t st;
     hipEvent_t done;
-  } mid{&qa, dims->head_dim, st, ev ? ev[3] : nullptr};
+  } mid{&qa2, dims->head_dim, st, ev ? ev[3] : nullptr};
   auto quant_between = [](void* c) -> hipError_t {
     const Mid* m = (const Mid*)c;
     hipError_t r = tp::launch_quantize(*m->qa, m->head_dim, m->st);
@@ -503,6 +569,8 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr, ev ? ev[5] : nullptr};
   if (e == hipSuccess)
     e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, quant_between, &mid);
+  // the selection reads the scales: wait for the lean kernel too
+  if (e == hipSuccess) e = hipStreamWaitEvent(st, aux->join, 0);
   if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
   if (e == hipSuccess) e = tp::launch_compact(ca, dims->num_layers * dims->num_kv_heads, dims->head_dim, st);

@@ -78,7 +78,87 @@ void launch_d(const QuantArgs& a, unsigned blocks, hipStream_t stream) {
   }
 }
 
+// ------------------------------------------------------------------ lean variant
+// The same quantisation with one workgroup per CU (one wave per SIMD) and at most 48 VGPRs,
+// so that it stays resident beside a score-pass workgroup (which leaves one wave slot and 48
+// VGPRs per SIMD free): each wave quantises kLeanLoads loads of RPW = 64/LPT consecutive rows
+// (1 KB each, coalesced), all loads issued before any row is quantised, then strides on.
+constexpr int kLeanLoads = 4;
+constexpr int kLeanBlocks = 256;
+
+template <int D, int K>
+__global__ __launch_bounds__(kQuantThreads) __attribute__((amdgpu_num_vgpr(48))) void k_quantize_lean(QuantArgs a) {
+  constexpr int LPT = D / 8;
+  constexpr int RPW = 64 / LPT;
+  constexpr int kWaves = kQuantThreads / 64;
+  const int lane = threadIdx.x & 63;
+  const int sub = lane % LPT;
+  const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
+  __shared__ QuantTables tab;
+  if (K != kScalesOnly) {
+    build_tables(tab, a.qmax);
+    __syncthreads();
+  }
+  const int64_t stride = (int64_t)gridDim.x * kWaves * kLeanLoads * RPW;
+  for (int64_t row0 = ((int64_t)blockIdx.x * kWaves + threadIdx.x / 64) * kLeanLoads * RPW; row0 < a.rows;
+       row0 += stride) {
+    uint4 x[kLeanLoads];
+#pragma unroll
+    for (int u = 0; u < kLeanLoads; ++u) {
+      const int64_t row = row0 + u * RPW + lane / LPT;
+      if (row < a.rows) {
+        const u32x4 t = __builtin_nontemporal_load((const u32x4*)(a.v + row * D) + sub);
+        x[u] = make_uint4(t.x, t.y, t.z, t.w);
+      } else {
+        x[u] = make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kLeanLoads; ++u) {
+      const int64_t row = row0 + u * RPW + lane / LPT;
+      if (K != kScalesOnly) {
+        uint2 c;
+        const float gamma = quant_piece<LPT, (K < 0 ? 0 : K)>(x[u], tab, f, c);
+        if (row >= a.rows) continue;
+        if (sub == 0) a.scales[row] = gamma;
+        store_codes<D, (K < 0 ? 0 : K)>(a.vq, row, sub, c);
+      } else {
+        const float gamma = scale_piece<LPT>(x[u], f);
+        if (row < a.rows && sub == 0) a.scales[row] = gamma;
+      }
+    }
+  }
+}
+
+template <int D>
+void launch_lean_d(const QuantArgs& a, hipStream_t stream) {
+  const dim3 grid(kLeanBlocks), block(kQuantThreads);
+  if (a.vq == nullptr) {
+    hipLaunchKernelGGL((k_quantize_lean<D, kScalesOnly>), grid, block, 0, stream, a);
+    return;
+  }
+  switch (qkind_of(a.qfmt, a.bits)) {
+    case kQByte:
+      hipLaunchKernelGGL((k_quantize_lean<D, kQByte>), grid, block, 0, stream, a);
+      break;
+    case kQNibble:
+      hipLaunchKernelGGL((k_quantize_lean<D, kQNibble>), grid, block, 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((k_quantize_lean<D, kQE4M3>), grid, block, 0, stream, a);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_quantize_lean(const QuantArgs& a, int head_dim, hipStream_t stream) {
+  if (a.rows <= 0) return hipSuccess;
+  if (head_dim == 128)
+    launch_lean_d<128>(a, stream);
+  else
+    launch_lean_d<64>(a, stream);
+  return hipGetLastError();
+}
 
 hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream) {
   const int lpt = head_dim / 8;

@@ -234,6 +234,7 @@ def test_evict_validation():
         (dict(ws=None), B.TP_ERR_WORKSPACE),
         (dict(wsb=1024), B.TP_ERR_WORKSPACE),
         (dict(sout=None, wsb=B.tp_workspace_size(B.TP_FN_GUIDE_SCORES, d, bt)), B.TP_ERR_WORKSPACE),
+        (dict(wsb=B.tp_workspace_size(B.TP_FN_EVICT, d, bt) - 1), B.TP_ERR_WORKSPACE),
         (dict(prof=short_prof), B.TP_ERR_PARAM),
         (dict(prof=null_prof), B.TP_ERR_NULL),
         (dict(k=FAKE + 8), B.TP_ERR_PARAM),
