@@ -64,7 +64,9 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
     # stream beside score pass 1 (k_quantize_lean); the k_quantize launch timed between the
     # events does the rest
     rows = LH * n
-    per["k_quantize"] = per["k_quantize"] * (rows - rows // 2 // 64 * 64) // rows
+    full = per["k_quantize"]
+    per["k_quantize"] = full * (rows - rows // 2 // 64 * 64) // rows
+    per["k_quantize_lean"] = full - per["k_quantize"]
     return per, path
 
 
