@@ -260,7 +260,8 @@ typedef struct tp_profile {
  * calls).  That stream and two events are created, with default priority, by the first
  * tp_evict call on a device and kept until the process ends (TP_ERR_HIP if that fails); the
  * work is forked from and joined back to `stream`, so the call stays stream-ordered and may
- * be captured into a graph.  Calls on one device enqueue one at a time (a lock held while
+ * be captured into a graph (once the first call on the device, which creates the stream,
+ * has been made outside capture).  Calls on one device enqueue one at a time (a lock held while
  * enqueueing, not while the work runs).
  * Every argument is validated before anything is enqueued.  Errors as for the four calls.
  */

@@ -542,6 +542,41 @@ def test_evict_with_supplied_normalisers_against_oracle(gpu_lib):
     pu.assert_scores_close(bufs.s_key.cpu().numpy(), own.s_key.cpu().numpy().astype(np.float64), "lse vs k_guide")
 
 
+def test_evict_graph_capture(gpu_lib):
+    """tp_evict captured into a graph (its second stream forks from and joins the capturing
+    stream) and replayed several times, with eager work and synchronisations between the
+    replays: every replay gives the eager outputs bit for bit."""
+    w = W.ragged8().with_(name="graph-replay", L=2, ctx_lens=(3000, 1, 4097), guide_lens=(32, 5, 64),
+                          keep_budget=300)
+    pu.log(f"tp_evict graph capture and replay: {w.describe()}")
+    q, k, v = pu.device_inputs(w)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=w.rule,
+              keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
+    eager = B.evict_fused(d, bt, q, k, v, **kw)  # also the first call on the device (outside capture)
+    torch.cuda.synchronize()
+    names = ("s_key", "scales", "v_q", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c")
+    ref = {n: getattr(eager, n).clone() for n in names}
+    ko = B.kept_offsets_for(bt, kw["keep_ratio"], kw["keep_budget"])
+    bufs = B.EvictBuffers(d, bt, w.qfmt, w.bits, ko)
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(graph, stream=cap):
+        B.evict_fused(d, bt, q, k, v, bufs=bufs, **kw)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for n in names:  # eager work between the replays
+            getattr(bufs, n).zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(bufs, n), ref[n]), (rep, n)
+        pu.log(f"  replay {rep} matches the eager call")
+
+
 def test_evict_without_full_codes(gpu_lib):
     """tp_evict with v_q = NULL (the kept rows are quantised during the compaction): the
     compact cache, kept set and scores are bit-identical to the run that writes every code."""
