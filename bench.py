@@ -141,9 +141,15 @@ def cpu_baseline(w, seconds: float):
     # a context token counts once all L * Hkv segments of it are done
     tokens_equiv = done_tokens / (w.L * w.Hkv)
     threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
+    cpu = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": tokens_equiv / elapsed, "unit": "context tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} of {len(segs)} (sequence, layer, KV head) segments, {elapsed:.1f} s of oracle time "
-                      f"(numpy float64; BLAS threads = cores)"}
+                      f"(numpy float64; BLAS threads = cores; {cpu}, {os.cpu_count()} logical CPUs visible)"}
 
 
 def machine_rates():
@@ -250,6 +256,9 @@ def main():
     ap.add_argument("--no-full-codes", action="store_true",
                     help="step 2 writes the scales only and the compaction quantises the kept V rows "
                          "(the codes of evicted rows are never written)")
+    ap.add_argument("--bits", type=int, default=None,
+                    help="integer code width b in [2, 8] instead of the workload's format (a b-sweep)")
+    ap.add_argument("--fp8", action="store_true", help="E4M3 codes instead of the workload's format")
     ap.add_argument("--rates", action="store_true",
                     help="only run the machine-ceiling microbenchmarks and print them")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -274,6 +283,10 @@ def main():
     from synth import workloads as W
 
     w = W.ALL[args.workload]()
+    if args.bits is not None:
+        w = w.with_(qfmt=B.TP_QFMT_INT, bits=args.bits)
+    if args.fp8:
+        w = w.with_(qfmt=B.TP_QFMT_FP8_E4M3, bits=8)
     torch.cuda.set_device(0)
     q, k, v = SD.device_inputs(w)
     kg = SD.device_guide_keys(w) if args.guide_keys else None
@@ -330,7 +343,9 @@ def main():
         return dict(roof, other_roof={k: other[k] for k in ("bound", "achieved", "unit", "frac")})
 
     kern = max(stage_ms, key=stage_ms.get)  # dominant kernel of the step
-    roofline = dict(roofline_of(kern), traffic=measured_traffic(kern, args.workload), kernel=kern,
+    # the committed counter summaries are of the workload's own format
+    same_fmt = args.bits is None and not args.fp8
+    roofline = dict(roofline_of(kern), traffic=measured_traffic(kern, args.workload) if same_fmt else None, kernel=kern,
                     avg_ms=round(stage_ms[kern], 4))
     path_gbs = path_bytes / (ms * 1e-3) / 1e9
     out = {
