@@ -159,11 +159,29 @@ __device__ inline void codes_fast(const uint32_t (&w)[4], float gamma, float ys,
     const float v = __uint_as_float(h);
     const float q0 = v * ys;
     const float y = fmaf(fmaf(-q0, gamma, v), ys, q0);
-    if (K == kQE4M3)
-      code[i] = e4m3_code(__builtin_copysignf(y, v));
-    else
-      code[i] = __float_as_uint(y + kRoundMagic);
+    code[i] = __float_as_uint(y + kRoundMagic);
   }
+}
+
+// E4M3 codes of 8 values on the common path, packed: the corrected quotient, clamped to
+// +-448 (it can exceed 448 by an ulp), with the sign of v (so -0 keeps its sign), converted
+// two at a time by the hardware fp32 -> OCP E4M3 conversion (nearest, ties to even,
+// subnormals kept); element 2i in byte 2i.
+__device__ inline uint2 codes_fast_e4m3(const uint32_t (&w)[4], float gamma, float ys) {
+  float y[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float v = __uint_as_float(h);
+    const float q0 = v * ys;
+    const float q = fmaf(fmaf(-q0, gamma, v), ys, q0);
+    y[i] = __builtin_copysignf(__builtin_amdgcn_fmed3f(q, -448.0f, 448.0f), v);
+  }
+  uint32_t lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], (int)lo, true);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[4], y[5], 0, false);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[6], y[7], (int)hi, true);
+  return make_uint2(lo, hi);
 }
 
 // Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
@@ -180,7 +198,12 @@ __device__ inline float quant_piece(const uint4& x, const QuantTables& tab, cons
   if (__builtin_amdgcn_ballot_w64(ef < kFastExpLo || ef > kFastExpHi) == 0) {
     const int t = (int)(mx & 0x7Fu);
     gamma = __builtin_amdgcn_ldexpf(tab.g[t], ef - 127);
-    codes_fast<K>(w, gamma, __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef), code);
+    const float ys = __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef);
+    if (K == kQE4M3) {
+      out = codes_fast_e4m3(w, gamma, ys);
+      return gamma;
+    }
+    codes_fast<K>(w, gamma, ys, code);
   } else {
     const float amax = __uint_as_float(mx << 16);
     gamma = amax / f.qmax;
