@@ -14,10 +14,12 @@
 // significand that the workgroup computes with IEEE divisions.  The quotient is
 // q0 = v * y' corrected once, fl(q0 + fma(-q0, gamma, v) * y'), and the integer code is the
 // low bits of that value plus 1.5 * 2^23 (an RNE round to an integer whose two's complement
-// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  Every
-// intermediate that can decide a code is a normal number in this range, and an exhaustive
-// check over every (A, v) pair of bf16 values, both signs, for every qmax of the supported
-// formats, gives the codes of the correctly rounded quotient.
+// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  An E4M3
+// code is the hardware conversion of that value clamped to +-448 (it can exceed 448 by an
+// ulp), with the sign of v.  Every intermediate that can decide a code is a normal number
+// in this range, and an exhaustive check over every (A, v) pair of bf16 values, both signs,
+// for every qmax of the supported formats, gives the codes of the correctly rounded
+// quotient.
 // Other rows (tiny, zero or huge absmax) take the general path: the row is rescaled by
 // 2^-e (e = exponent of the absmax), the same corrected quotient is formed against
 // gamma' = gamma * 2^-e with one division per row, and the code is rounded and clamped
