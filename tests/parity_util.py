@@ -62,12 +62,15 @@ def oracle_guide_lse(w, guide_keys=False, jitter_seed=None):
     return out.astype(np.float32)
 
 
-def run_gpu(w, q, k, v, rule=None, bufs=None, k_guide=None):
+def run_gpu(w, q, k, v, rule=None, bufs=None, k_guide=None, fused=False):
+    """The path on workload w: the four entry points one after the other, or (fused=True)
+    tp_evict, the launch configuration the bench times."""
     d = B.dims(w.L, w.Hq, w.Hkv, w.d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
-    out = B.evict(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
-                  rule=w.rule if rule is None else rule, keep_ratio=w.keep_ratio or 0.0,
-                  keep_budget=w.keep_budget or 0, bufs=bufs, k_guide=k_guide)
+    run = B.evict_fused if fused else B.evict
+    out = run(d, bt, q, k, v, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
+              rule=w.rule if rule is None else rule, keep_ratio=w.keep_ratio or 0.0,
+              keep_budget=w.keep_budget or 0, bufs=bufs, k_guide=k_guide)
     torch.cuda.synchronize()
     return out
 

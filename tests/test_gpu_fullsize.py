@@ -51,7 +51,7 @@ def test_fullsize_sampled(gpu_lib, name):
     pu.log(f"full size: {w.describe()}")
     torch.cuda.empty_cache()
     q, k, v = pu.device_inputs(w)
-    bufs = pu.run_gpu(w, q, k, v)
+    bufs = pu.run_gpu(w, q, k, v, fused=True)  # tp_evict, as the bench runs it
     _properties_all_segments(w, bufs)
     for (b, l, h) in SAMPLES[name]:
         pu.log(f"  oracle segment b={b} l={l} h={h}")
