@@ -20,8 +20,9 @@
  *  - Tensor pointers are DEVICE pointers; shape / offset arrays are HOST pointers.
  *    `stream` is a hipStream_t (NULL = the default stream).
  *  - Ownership: the caller allocates every input, output and workspace buffer.
- *    The library allocates nothing and keeps no pointer after returning; buffers
- *    must stay valid until the enqueued work has completed.
+ *    The library allocates no memory and keeps no pointer after returning; buffers
+ *    must stay valid until the enqueued work has completed.  (tp_evict keeps one
+ *    stream and two events of its own per device: see tp_evict.)
  *  - Execution is asynchronous and stream-ordered; nothing synchronises inside a
  *    call.  Calls are re-entrant.  Results are bit-identical from run to run (no
  *    floating-point atomics; fixed reduction orders).
