@@ -29,6 +29,7 @@ namespace tp {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 union Frag {
@@ -416,45 +417,68 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_stats(GuideArgs a) {
   }
 }
 
-// ---------------------------------------------------------------------------- lse merge
-// One thread per guide row: merge the row's per-chunk (max, sum) pairs into lse2.  With the
-// guide's own keys (the paper-literal slice of the causal attention over context + appended
-// guide, Sec. 3.2), row j's normaliser also takes the logits of guide keys 0..j, computed
-// here (d products per key, fp32).
+// ---------------------------------------------------------------------------- guide keys
+// With the guide's own keys (the paper-literal slice of the causal attention over context +
+// appended guide, Sec. 3.2), guide row j's normaliser also takes the logits of guide keys
+// 0..j.  One workgroup takes up to 256 guide rows of a (sequence, layer, KV head); the
+// guide keys of that head are staged in LDS kGuideKeyTile at a time, and every lane (one
+// row each, its query in registers) walks the keys in the same order, so all lanes read the
+// same key row at once (an LDS broadcast).  The row's (max, sum) over its keys t <= j goes
+// to the extra statistics slot nchunk_max, which the merge below treats as one more chunk.
+constexpr int kGuideKeyTile = 64;
+
 template <int D>
-__device__ inline void guide_key_terms(const GuideArgs& a, int64_t grow, int64_t l, int64_t qh, int64_t g0, int64_t j,
-                                       float& m, float& s) {
-  const int64_t h = qh / a.R;
-  const uint4* qrow = (const uint4*)(a.q + grow * D);
-  float qf[D];
+__global__ __launch_bounds__(256) void k_guide_key_stats(GuideArgs a) {
+  const int b = blockIdx.z, seg = blockIdx.y;
+  const int64_t g0 = a.bt.g_off[b];
+  const int gb = (int)(a.bt.g_off[b + 1] - g0);
+  const int rows = a.R * gb;
+  const int rho = blockIdx.x * 256 + threadIdx.x;  // guide row of the segment: (r, j)
+  if ((int)blockIdx.x * 256 >= rows) return;       // the whole block has no rows
+  const int64_t l = seg / a.Hkv, h = seg % a.Hkv;
+  const bool live = rho < rows;
+  const int r = live ? rho / gb : 0, j = live ? rho % gb : -1;
+  const int64_t grow = ((l * a.Hq + h * a.R + r) * a.g_tot) + g0 + (live ? j : 0);
+  __shared__ uint4 keys[kGuideKeyTile][D / 8];
+  uint4 qv[D / 8];  // the row's query, bf16 pairs
+  {
+    const uint4* qrow = (const uint4*)(a.q + grow * D);
 #pragma unroll
-  for (int p = 0; p < D / 8; ++p) {
-    const uint4 u = qrow[p];
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qf[8 * p + 2 * e] = __uint_as_float(w[e] << 16);
-      qf[8 * p + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-    }
+    for (int p = 0; p < D / 8; ++p) qv[p] = qrow[p];
   }
-  const uint16_t* kg = a.kg + ((l * a.Hkv + h) * a.g_tot + g0) * D;
-  for (int64_t t = 0; t <= j; ++t) {
-    const uint4* krow = (const uint4*)(kg + t * D);
-    float dot = 0.f;
+  // the block's rows need keys 0 .. max j; its last row has the largest j unless it wraps
+  const int last = min(rows, (int)(blockIdx.x + 1) * 256) - 1;
+  const int nkeys = ((int)blockIdx.x * 256) / gb == last / gb ? last % gb + 1 : gb;
+  const uint4* kg = (const uint4*)(a.kg + ((l * a.Hkv + h) * a.g_tot + g0) * D);
+  float m = kNoMax, s = 0.f;
+  for (int t0 = 0; t0 < nkeys; t0 += kGuideKeyTile) {
+    const int nt = min(kGuideKeyTile, nkeys - t0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < nt * (D / 8); i += 256) keys[i / (D / 8)][i % (D / 8)] = kg[(int64_t)(t0 + i / (D / 8)) * (D / 8) + i % (D / 8)];
+    __syncthreads();
+    const int tend = min(nt, j - t0 + 1);  // keys t0 .. j of this tile (none for idle lanes)
+    for (int t = 0; t < tend; ++t) {
+      // fp32 dot product of bf16 pairs (v_dot2_f32_bf16), four independent partial sums
+      float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < D / 8; ++p) {
-      const uint4 u = krow[p];
-      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+      for (int p = 0; p < D / 8; ++p) {
+        const uint4 u = keys[t][p];
+        const uint32_t kw[4] = {u.x, u.y, u.z, u.w};
+        const uint32_t qw[4] = {qv[p].x, qv[p].y, qv[p].z, qv[p].w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dot = fmaf(qf[8 * p + 2 * e], __uint_as_float(w[e] << 16), dot);
-        dot = fmaf(qf[8 * p + 2 * e + 1], __uint_as_float(w[e] & 0xFFFF0000u), dot);
+        for (int e = 0; e < 4; ++e)
+          part[e] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw[e]),
+                                                    __builtin_bit_cast(bf16x2, kw[e]), part[e], false);
       }
+      merge_stats(m, s, ((part[0] + part[1]) + (part[2] + part[3])) * a.c, 1.0f);
     }
-    merge_stats(m, s, dot * a.c, 1.0f);
   }
+  if (live) a.stats[(int64_t)a.nchunk_max * ((int64_t)a.L * a.Hq * a.g_tot) + grow] = make_float2(m, s);
 }
 
+// ---------------------------------------------------------------------------- lse merge
+// One thread per guide row: merge the row's per-chunk (max, sum) pairs (and, with guide
+// keys, the guide-key slot) into lse2.
 template <int D>
 __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
   const int b = blockIdx.y;
@@ -474,7 +498,10 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
     const float2 v = a.stats[(int64_t)c * growtot + grow];
     merge_stats(m, s, v.x, v.y);
   }
-  if (a.kg != nullptr) guide_key_terms<D>(a, grow, l, qh, g0, j, m, s);
+  if (a.kg != nullptr) {
+    const float2 v = a.stats[(int64_t)a.nchunk_max * growtot + grow];
+    merge_stats(m, s, v.x, v.y);
+  }
   a.lse2[grow] = m + log2f(s);
 }
 
@@ -717,6 +744,10 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, Guid
     if (e == hipSuccess && ev) e = hipEventRecord(ev[pass == 0 ? 0 : 2], stream);
     if (e != hipSuccess) return e;
     if (pass == 0) {
+      if (a.kg != nullptr) {
+        const dim3 kgrid((unsigned)((a.R * max_gb + 255) / 256), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
+        hipLaunchKernelGGL(k_guide_key_stats<D>, kgrid, dim3(256), 0, stream, a);
+      }
       const dim3 lgrid((unsigned)((a.L * a.Hq * max_gb + 255) / 256), (unsigned)a.bt.batch);
       hipLaunchKernelGGL(k_guide_lse<D>, lgrid, dim3(256), 0, stream, a);
       e = hipGetLastError();
@@ -747,8 +778,8 @@ GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const 
   const int64_t nrg = (R * max_gb + kRowsPerGroup - 1) / kRowsPerGroup;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   GuideWorkspace w;
-  w.stats_off = 0;
-  w.lse_off = up((size_t)nchunk * L * Hq * g_tot * sizeof(float2));
+  w.stats_off = 0;  // nchunk slots of per-chunk statistics, plus one for the guide keys
+  w.lse_off = up((size_t)(nchunk + 1) * L * Hq * g_tot * sizeof(float2));
   w.raw_off = w.lse_off + up((size_t)L * Hq * g_tot * sizeof(float));
   w.total = w.raw_off + up((size_t)nrg * L * Hkv * n_tot * sizeof(float));
   return w;

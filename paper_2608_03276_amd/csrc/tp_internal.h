@@ -28,7 +28,8 @@ struct GuideArgs {
   const uint16_t* kg; // bf16 [L][Hkv][G_tot][d] guide keys, or nullptr (context-only normaliser)
   const float* lse_in;// fp32 [L][Hq][G_tot] caller's natural-log row normalisers, or nullptr
   float* s_key;       // fp32 [L][Hkv][N_tot]
-  float2* stats;      // [nchunk_max][L*Hq*G_tot]   per-chunk (max, sum) in the log2 domain
+  float2* stats;      // [nchunk_max + 1][L*Hq*G_tot] per-chunk (max, sum) in the log2 domain;
+                      //   slot nchunk_max: the guide keys' terms (with kg)
   float* lse2;        // [L*Hq*G_tot]               log2-sum-exp2 of the row's normaliser
   float* raw;         // [nrg_max][L*Hkv][N_tot]    per row-group sums of normalised attention
   int32_t L, Hq, Hkv, R;
