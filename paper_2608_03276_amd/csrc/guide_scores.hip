@@ -625,7 +625,7 @@ __global__ __launch_bounds__(kGuideThreads, 1) void k_guide_attn(GuideArgs a) {
 // sequence).  A block stages kPoolTile + 2*half raw values (summed over row groups) in LDS
 // with coalesced loads, then each thread sums its windows from LDS; windows wider than
 // kPoolMaxHalf use the direct loop.
-constexpr int kPoolTile = 2048;
+constexpr int kPoolTile = 4096;
 constexpr int kPoolMaxHalf = 512;
 
 __device__ inline float raw_at(const GuideArgs& a, const float* raw, int nrg, int64_t j) {
