@@ -110,10 +110,10 @@ def copy_calibration(gib: float = 1.0, reps: int = 3):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
-def cpu_baseline(w, seconds: float):
-    """The CPU oracle (test infrastructure) timed on a bounded sample of segments."""
+def _oracle_rate(w, seconds: float, seed: int):
+    """(context tokens/s, segments done, oracle seconds) of the CPU oracle on a random sample
+    of (sequence, layer, KV head) segments; input generation is not timed."""
     import numpy as np
-    import threadpoolctl
 
     from oracle import taskpress_oracle as o
 
@@ -121,14 +121,13 @@ def cpu_baseline(w, seconds: float):
     import parity_util as pu
 
     segs = [(b, l, h) for b in range(w.batch) for l in range(w.L) for h in range(w.Hkv)]
-    rng = np.random.default_rng(0)
-    order = rng.permutation(len(segs))
+    order = np.random.default_rng(seed).permutation(len(segs))
     done_tokens = 0
     done = 0
     elapsed = 0.0
     for i in order:
         b, l, h = segs[i]
-        qg, kb, vb = pu.host_segment(w, b, l, h)  # input generation is not timed
+        qg, kb, vb = pu.host_segment(w, b, l, h)
         k = o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget)
         t0 = time.perf_counter()
         o.evict_segment(qg, kb, vb, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
@@ -139,7 +138,18 @@ def cpu_baseline(w, seconds: float):
         if elapsed >= seconds:
             break
     # a context token counts once all L * Hkv segments of it are done
-    tokens_equiv = done_tokens / (w.L * w.Hkv)
+    return done_tokens / (w.L * w.Hkv) / elapsed, done, elapsed
+
+
+def cpu_baseline(w, seconds: float):
+    """The CPU oracle (test infrastructure) timed on a bounded sample of segments, with the
+    host's BLAS threads and with one thread."""
+    import threadpoolctl
+
+    segs = w.batch * w.L * w.Hkv
+    rate, done, elapsed = _oracle_rate(w, seconds, 0)
+    with threadpoolctl.threadpool_limits(limits=1):
+        rate1, done1, elapsed1 = _oracle_rate(w, seconds / 3, 1)
     threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
     cpu = "unknown CPU"
     try:
@@ -147,9 +157,12 @@ def cpu_baseline(w, seconds: float):
             cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
         pass
-    return {"value": tokens_equiv / elapsed, "unit": "context tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {len(segs)} (sequence, layer, KV head) segments, {elapsed:.1f} s of oracle time "
-                      f"(numpy float64; BLAS threads = cores; {cpu}, {os.cpu_count()} logical CPUs visible)"}
+    return {"value": rate, "unit": "context tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {segs} (sequence, layer, KV head) segments, {elapsed:.1f} s of oracle time "
+                      f"(numpy float64; BLAS threads = cores; {cpu}, {os.cpu_count()} logical CPUs visible)",
+            "value_1_thread": rate1,
+            "sample_1_thread": f"{done1} segments (another random order), {elapsed1:.1f} s of oracle time, BLAS "
+                               f"limited to 1 thread"}
 
 
 def machine_rates():
