@@ -577,6 +577,49 @@ def test_evict_graph_capture(gpu_lib):
         pu.log(f"  replay {rep} matches the eager call")
 
 
+def test_evict_concurrent_threads(gpu_lib):
+    """Two host threads calling tp_evict at the same time, each on its own stream with its
+    own buffers (the calls share the device's second stream and events, whose use is
+    serialised by a lock while enqueueing): every result equals the serial call's."""
+    import threading
+
+    w = W.ragged8().with_(name="threads", L=2, ctx_lens=(3000, 1, 4097), guide_lens=(32, 5, 64), keep_budget=300)
+    pu.log(f"tp_evict from two threads: {w.describe()}")
+    q, k, v = pu.device_inputs(w)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=w.rule,
+              keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
+    names = ("s_key", "scales", "v_q", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c")
+    ref = B.evict_fused(d, bt, q, k, v, **kw)
+    torch.cuda.synchronize()
+    ko = B.kept_offsets_for(bt, kw["keep_ratio"], kw["keep_budget"])
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    bufs = [B.EvictBuffers(d, bt, w.qfmt, w.bits, ko) for _ in streams]
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    errors = []
+
+    def worker(i):
+        try:
+            for _ in range(5):
+                B.evict_fused(d, bt, q, k, v, bufs=bufs[i], stream=streams[i], **kw)
+            streams[i].synchronize()
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for i in range(2):
+        for n in names:
+            assert torch.equal(getattr(bufs[i], n), getattr(ref, n)), (i, n)
+
+
 def test_evict_without_full_codes(gpu_lib):
     """tp_evict with v_q = NULL (the kept rows are quantised during the compaction): the
     compact cache, kept set and scores are bit-identical to the run that writes every code."""
