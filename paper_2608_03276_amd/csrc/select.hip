@@ -23,7 +23,7 @@ namespace {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kPerThread = 4;
-constexpr int kBatch = 8;  // keys each thread loads before it touches the histogram
+constexpr int kBatch = 16;  // keys each thread loads before it touches the histogram
 constexpr int kTopBits = 12;              // first digit: bits 31..20 of the key
 constexpr int kBins = 1 << kTopBits;      // histogram bins (the 8-bit last digit uses 256)
 constexpr int kCandCap = 16384;           // keys of the threshold's top-digit bucket held in LDS
