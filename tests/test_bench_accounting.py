@@ -1,0 +1,46 @@
+"""The algorithmic byte counts bench.py divides by the measured times (CPU only): the whole
+path's bytes follow the compulsory-traffic formula per (layer, KV head, context token) at
+d = 128 — read K and V once, write the 8-bit codes and the fp32 scale (644 B), plus per
+kept token the re-read of its K row, codes and scale and the write of the compact cache and
+index (780 B) — and the per-kernel counts of step 2 add up over its two launches."""
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from synth import workloads as W  # noqa: E402
+
+
+def _kept(w):
+    from oracle import taskpress_oracle as o
+
+    return sum(o.keep_count(n, w.keep_ratio, w.keep_budget) for n in w.ctx_lens)
+
+
+def test_path_bytes_128k():
+    w = W.llama8b_128k()
+    k = _kept(w)
+    assert k == 13107
+    per, path = bench.algorithmic_bytes(w, k)
+    LH, n = w.L * w.Hkv, w.n_tot
+    q_bytes = w.L * w.Hq * w.g_tot * w.d * 2
+    assert path == LH * (644 * n + 780 * k) + q_bytes
+    assert abs(path / 1e9 - 24.24) < 0.01
+    # step 2's two launches (the second-stream half and the rest) cover every V row once
+    assert per["k_quantize"] + per["k_quantize_lean"] == LH * n * (2 * w.d + w.d + 4)
+
+
+def test_path_bytes_scales_only_and_int4():
+    w = W.llama8b_128k()
+    k = _kept(w)
+    LH, n = w.L * w.Hkv, w.n_tot
+    q_bytes = w.L * w.Hq * w.g_tot * w.d * 2
+    _, path = bench.algorithmic_bytes(w, k, full_codes=False)
+    # scales only (516 B per token-head), the kept rows re-read in bf16 and quantised
+    assert path == LH * (516 * n + k * (256 + 256 + 4 + 256 + 128 + 4)) + q_bytes
+    w4 = w.with_(bits=4)
+    _, path4 = bench.algorithmic_bytes(w4, k)
+    assert path4 == LH * ((256 + 256 + 64 + 4) * n + k * (2 * (256 + 64 + 4) + 4)) + q_bytes
