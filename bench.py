@@ -44,7 +44,8 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
     kt = kept_total_per_head
     q_bytes = w.L * w.Hq * w.g_tot * d * 2
     rows = w.L * w.Hq * w.g_tot
-    nch = -(-max(w.ctx_lens) // 8192)
+    chunk = 16384 if min(w.ctx_lens) >= 65536 else 8192  # the score passes' chunk (tp_internal.h)
+    nch = -(-max(w.ctx_lens) // chunk)
     per = {
         "k_guide_stats": LH * n * 2 * d + q_bytes + rows * nch * 8,     # read K, write chunk stats
         "k_guide_lse": rows * (nch * 8 + 4),                            # merge chunk stats

@@ -160,7 +160,8 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   a.c = (float)((double)softmax_scale * 1.4426950408889634);
   a.pool_inv = (float)(1.0 / ((double)a.R * pool_k));
   a.pool_half = pool_k / 2;
-  a.nchunk_max = (int32_t)((max_nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
+  a.chunk = tp::chunk_tokens(batch->ctx_offsets, batch->batch);
+  a.nchunk_max = (int32_t)((max_nb + a.chunk - 1) / a.chunk);
   a.nrg_max = (int32_t)((a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
   // workgroups of the score passes (the launcher splits them into row-block classes, each
   // with its own per-sequence ranges in wg_off); the total must fit one grid
@@ -169,7 +170,7 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
   for (int b = 0; b < batch->batch; ++b) {
     const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
     const int64_t gb = batch->guide_offsets[b + 1] - batch->guide_offsets[b];
-    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + tp::kChunkTokens - 1) / tp::kChunkTokens);
+    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + a.chunk - 1) / a.chunk);
     wg += (units + 7) / 8 * 8 * ((a.R * gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup);
     if (wg > 0x7FFFFFFF) return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
     a.wg_off[b + 1] = (int32_t)wg;

@@ -45,7 +45,6 @@ struct Cfg {
   static constexpr int kStride = kRowBytes + 16;         // LDS bytes per staged query row
   static constexpr int kStageBytes = 32 * kRowBytes;     // one K sub-tile
   static constexpr int kTokPerKB = 1024 / kRowBytes;     // tokens per 1 KB copy instruction
-  static constexpr int kSubPerWave = kChunkTokens / 32 / kGuideWaves;
 };
 
 struct Work {
@@ -73,7 +72,7 @@ __device__ inline bool decode(const GuideArgs& a, Work& w) {
   w.gb = (int)(a.bt.g_off[b + 1] - w.g0);
   w.rows = a.R * w.gb;
   const int nrg = (w.rows + kRowsPerGroup - 1) / kRowsPerGroup;
-  const int nchunk = (int)((w.nb + kChunkTokens - 1) / kChunkTokens);
+  const int nchunk = (int)((w.nb + a.chunk - 1) / a.chunk);
   const int xcd = xb & 7, slot = xb >> 3;
   w.rg = slot % nrg;
   const int64_t unit = (int64_t)(slot / nrg) * 8 + xcd;
@@ -82,8 +81,8 @@ __device__ inline bool decode(const GuideArgs& a, Work& w) {
   w.chunk = (int)(unit % nchunk);
   w.l = w.seg / a.Hkv;
   w.h = w.seg % a.Hkv;
-  w.c0 = (int64_t)w.chunk * kChunkTokens;
-  w.c1 = w.c0 + kChunkTokens < w.nb ? w.c0 + kChunkTokens : w.nb;
+  w.c0 = (int64_t)w.chunk * a.chunk;
+  w.c1 = w.c0 + a.chunk < w.nb ? w.c0 + a.chunk : w.nb;
   w.row0 = w.rg * kRowsPerGroup;
   w.nrows = w.rows - w.row0 < kRowsPerGroup ? w.rows - w.row0 : kRowsPerGroup;
   return true;
@@ -492,7 +491,7 @@ __global__ __launch_bounds__(256) void k_guide_lse(GuideArgs a) {
   const int64_t qh = rem / gb, j = rem - qh * gb;
   const int64_t grow = (l * a.Hq + qh) * a.g_tot + g0 + j;
   const int64_t growtot = (int64_t)a.L * a.Hq * a.g_tot;
-  const int nch = (int)((nb + kChunkTokens - 1) / kChunkTokens);
+  const int nch = (int)((nb + a.chunk - 1) / a.chunk);
   float m = kNoMax, s = 0.f;
   for (int c = 0; c < nch; ++c) {
     const float2 v = a.stats[(int64_t)c * growtot + grow];
@@ -706,7 +705,7 @@ hipError_t launch_pass(const GuideArgs& a, bool attn, hipStream_t stream) {
 // arguments give the other sequences empty workgroup ranges.
 template <int D>
 hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, GuideBetween between, void* ctx) {
-  static_assert(Cfg<D>::kSubPerWave >= 1, "chunk too small");
+  static_assert(kChunkSmall % (32 * kGuideWaves) == 0, "every wave owns whole sub-tiles of a chunk");
   int64_t max_nb = 0, max_gb = 0;
   GuideArgs cls[4];
   int64_t wg[4] = {0, 0, 0, 0};
@@ -721,7 +720,7 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, Guid
     if (gb > max_gb) max_gb = gb;
     const int64_t rows = (int64_t)a.R * gb;
     const int np = (int)(((rows < kRowsPerGroup ? rows : kRowsPerGroup) + 63) / 64);
-    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + kChunkTokens - 1) / kChunkTokens);
+    const int64_t units = (int64_t)a.L * a.Hkv * ((nb + a.chunk - 1) / a.chunk);
     wg[np - 1] += (units + 7) / 8 * 8 * ((rows + kRowsPerGroup - 1) / kRowsPerGroup);
     for (int c = 0; c < 4; ++c) cls[c].wg_off[b + 1] = (int32_t)wg[c];
   }
@@ -774,7 +773,8 @@ GuideWorkspace guide_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, const 
   }
   const int64_t n_tot = ctx_off[batch], g_tot = g_off[batch];
   const int64_t R = Hq / Hkv;
-  const int64_t nchunk = (max_nb + kChunkTokens - 1) / kChunkTokens;
+  const int64_t chunk = chunk_tokens(ctx_off, batch);
+  const int64_t nchunk = (max_nb + chunk - 1) / chunk;
   const int64_t nrg = (R * max_gb + kRowsPerGroup - 1) / kRowsPerGroup;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   GuideWorkspace w;

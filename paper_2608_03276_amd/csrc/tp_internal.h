@@ -20,7 +20,18 @@ struct BatchArgs {
 constexpr int kGuideThreads = 512;       // 8 waves of 64, two per SIMD
 constexpr int kGuideWaves = kGuideThreads / 64;
 constexpr int kRowsPerGroup = 256;       // guide rows handled by one workgroup
-constexpr int kChunkTokens = 8192;       // tokens of one segment per workgroup
+// Context tokens of one segment per score-pass workgroup (a "chunk"): 16384 when every
+// sequence of the batch has at least 65536 context tokens, so the per-workgroup query
+// staging and statistics merge are spread over more tokens; else 8192, so short and ragged
+// sequences keep enough workgroups and little padding.
+constexpr int kChunkSmall = 8192;
+constexpr int kChunkLarge = 16384;
+constexpr int64_t kLongContext = 65536;
+inline int32_t chunk_tokens(const int64_t* ctx_off, int32_t batch) {
+  for (int b = 0; b < batch; ++b)
+    if (ctx_off[b + 1] - ctx_off[b] < kLongContext) return kChunkSmall;
+  return kChunkLarge;
+}
 
 struct GuideArgs {
   const uint16_t* q;  // bf16 [L][Hq][G_tot][d]
@@ -37,6 +48,7 @@ struct GuideArgs {
   float c;            // softmax_scale * log2(e)
   float pool_inv;     // 1 / (R * pool_k)
   int32_t pool_half;  // pool_k / 2
+  int32_t chunk;      // context tokens per chunk (chunk_tokens of the batch)
   int32_t nchunk_max; // chunks of the longest sequence
   int32_t nrg_max;    // row groups of the largest R * G_b
   BatchArgs bt;
