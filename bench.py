@@ -273,6 +273,8 @@ def main():
     ap.add_argument("--bits", type=int, default=None,
                     help="integer code width b in [2, 8] instead of the workload's format (a b-sweep)")
     ap.add_argument("--fp8", action="store_true", help="E4M3 codes instead of the workload's format")
+    ap.add_argument("--guide-tokens", type=int, default=None,
+                    help="guide length G of every sequence instead of the workload's (a guide-length sweep)")
     ap.add_argument("--rates", action="store_true",
                     help="only run the machine-ceiling microbenchmarks and print them")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -301,6 +303,8 @@ def main():
         w = w.with_(qfmt=B.TP_QFMT_INT, bits=args.bits)
     if args.fp8:
         w = w.with_(qfmt=B.TP_QFMT_FP8_E4M3, bits=8)
+    if args.guide_tokens is not None:
+        w = w.with_(guide_lens=tuple(args.guide_tokens for _ in w.ctx_lens))
     torch.cuda.set_device(0)
     q, k, v = SD.device_inputs(w)
     kg = SD.device_guide_keys(w) if args.guide_keys else None
@@ -358,7 +362,7 @@ def main():
 
     kern = max(stage_ms, key=stage_ms.get)  # dominant kernel of the step
     # the committed counter summaries are of the workload's own format
-    same_fmt = args.bits is None and not args.fp8
+    same_fmt = args.bits is None and not args.fp8 and args.guide_tokens is None
     roofline = dict(roofline_of(kern), traffic=measured_traffic(kern, args.workload) if same_fmt else None, kernel=kern,
                     avg_ms=round(stage_ms[kern], 4))
     path_gbs = path_bytes / (ms * 1e-3) / 1e9

@@ -693,10 +693,11 @@ template <int D, int NP>
 hipError_t launch_pass(const GuideArgs& a, bool attn, hipStream_t stream) {
   const unsigned nwg = (unsigned)a.wg_off[a.bt.batch];
   if (nwg == 0) return hipSuccess;
-  if (attn)
+  if (attn) {
     hipLaunchKernelGGL((k_guide_attn<D, NP>), dim3(nwg), dim3(kGuideThreads), 0, stream, a);
-  else
+  } else if constexpr (NP != 3) {  // pass 1 has no 3-pair class (see launch_d)
     hipLaunchKernelGGL((k_guide_stats<D, NP>), dim3(nwg), dim3(kGuideThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
@@ -707,12 +708,18 @@ template <int D>
 hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, GuideBetween between, void* ctx) {
   static_assert(kChunkSmall % (32 * kGuideWaves) == 0, "every wave owns whole sub-tiles of a chunk");
   int64_t max_nb = 0, max_gb = 0;
-  GuideArgs cls[4];
-  int64_t wg[4] = {0, 0, 0, 0};
-  for (int c = 0; c < 4; ++c) {
-    cls[c] = a;
-    cls[c].wg_off[0] = 0;
-  }
+  // per pass and class NP (1..4 staged row-block pairs) the launch arguments, with the other
+  // classes' sequences given empty workgroup ranges.  Pass 1 has no NP = 3 class: its
+  // three-pair kernel needs more VGPRs than the four-pair one (248 against 228) and would
+  // leave no room for the quantisation tp_evict runs beside pass 1, so 129..192 rows are
+  // padded to four pairs there (the padding rows' statistics are never stored).
+  GuideArgs cls[2][4];
+  int64_t wg[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+  for (int pass = 0; pass < 2; ++pass)
+    for (int c = 0; c < 4; ++c) {
+      cls[pass][c] = a;
+      cls[pass][c].wg_off[0] = 0;
+    }
   for (int b = 0; b < a.bt.batch; ++b) {
     const int64_t nb = a.bt.ctx_off[b + 1] - a.bt.ctx_off[b];
     const int64_t gb = a.bt.g_off[b + 1] - a.bt.g_off[b];
@@ -721,8 +728,11 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, Guid
     const int64_t rows = (int64_t)a.R * gb;
     const int np = (int)(((rows < kRowsPerGroup ? rows : kRowsPerGroup) + 63) / 64);
     const int64_t units = (int64_t)a.L * a.Hkv * ((nb + a.chunk - 1) / a.chunk);
-    wg[np - 1] += (units + 7) / 8 * 8 * ((rows + kRowsPerGroup - 1) / kRowsPerGroup);
-    for (int c = 0; c < 4; ++c) cls[c].wg_off[b + 1] = (int32_t)wg[c];
+    const int64_t seq_wg = (units + 7) / 8 * 8 * ((rows + kRowsPerGroup - 1) / kRowsPerGroup);
+    wg[0][np == 3 ? 3 : np - 1] += seq_wg;
+    wg[1][np - 1] += seq_wg;
+    for (int pass = 0; pass < 2; ++pass)
+      for (int c = 0; c < 4; ++c) cls[pass][c].wg_off[b + 1] = (int32_t)wg[pass][c];
   }
   for (int pass = 0; pass < 2; ++pass) {  // the large classes first: shorter tail
     if (pass == 0 && a.lse_in) {  // normalisers given: no pass 1
@@ -736,10 +746,10 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, Guid
       if (e != hipSuccess) return e;
       continue;
     }
-    hipError_t e = launch_pass<D, 4>(cls[3], pass == 1, stream);
-    if (e == hipSuccess) e = launch_pass<D, 3>(cls[2], pass == 1, stream);
-    if (e == hipSuccess) e = launch_pass<D, 2>(cls[1], pass == 1, stream);
-    if (e == hipSuccess) e = launch_pass<D, 1>(cls[0], pass == 1, stream);
+    hipError_t e = launch_pass<D, 4>(cls[pass][3], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 3>(cls[pass][2], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 2>(cls[pass][1], pass == 1, stream);
+    if (e == hipSuccess) e = launch_pass<D, 1>(cls[pass][0], pass == 1, stream);
     if (e == hipSuccess && ev) e = hipEventRecord(ev[pass == 0 ? 0 : 2], stream);
     if (e != hipSuccess) return e;
     if (pass == 0) {
