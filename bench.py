@@ -23,18 +23,24 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 
 # The kernels of one tp_evict call, in launch order (the library records an event after each).
 STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_guide_pool", "k_select", "k_compact"]
-KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip"], "k_guide_lse": ["guide_scores.hip"],
-                  "k_guide_attn": ["guide_scores.hip"], "k_guide_pool": ["guide_scores.hip"],
-                  "k_quantize": ["quantize.hip", "quant_row.h"], "k_quantize_lean": ["quantize.hip", "quant_row.h"],
-                  "k_select": ["select.hip"],
-                  "k_compact": ["compact.hip"], "k_compact_quant": ["compact.hip", "quant_row.h"],
-                  "k_lse_import": ["guide_scores.hip"]}
+KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
+                  "k_guide_lse": ["guide_scores.hip", "tp_internal.h"],
+                  "k_guide_attn": ["guide_scores.hip", "tp_internal.h"],
+                  "k_guide_pool": ["guide_scores.hip", "tp_internal.h"],
+                  # the rows each step-2 launch takes are set by tp_evict
+                  "k_quantize": ["quantize.hip", "quant_row.h", "tp_internal.h", "abi.cpp"],
+                  "k_quantize_lean": ["quantize.hip", "quant_row.h", "tp_internal.h", "abi.cpp"],
+                  "k_select": ["select.hip", "tp_internal.h"],
+                  "k_compact": ["compact.hip", "tp_internal.h"],
+                  "k_compact_quant": ["compact.hip", "quant_row.h", "tp_internal.h"],
+                  "k_lse_import": ["guide_scores.hip", "tp_internal.h"]}
 
 
-def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
-    """Compulsory HBM bytes of each kernel of the step and of the whole path (see the design
-    notes).  A kernel's bytes are what it must move itself; the path counts K once.  Without
-    full codes step 2 writes the scales only and the compaction re-reads the kept V rows."""
+def algorithmic_bytes(w, kept_total_per_head, full_codes=True, normalisers_given=False):
+    """Compulsory HBM bytes of each kernel launch of the step and of the whole path (see the
+    design notes).  A kernel's bytes are what it must move itself; the path counts K once.
+    Without full codes step 2 writes the scales only and the compaction re-reads the kept V
+    rows.  Every kernel is launched once per step except k_quantize_lean (LEAN_LAUNCHES)."""
     from paper_2608_03276_amd import binding as B
 
     LH = w.L * w.Hkv
@@ -61,14 +67,21 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True):
     if not full_codes:
         per["k_quantize"] = LH * n * (2 * d + 4)                        # read V, write scales
         path = LH * (n * (2 * d + 2 * d + 4) + kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4)) + q_bytes
-    # tp_evict quantises the first half of the V rows (rounded down to 64 rows) on its second
-    # stream beside score pass 1 (k_quantize_lean); the k_quantize launch timed between the
-    # events does the rest
+    # tp_evict quantises a third of the V rows (rounded down to 64 rows) on its second stream
+    # beside each score pass (two k_quantize_lean launches), or, with the normalisers given, the
+    # first half beside nothing but the rest of the step (one launch); the k_quantize launch timed
+    # between the events does the rest
     rows = LH * n
     full = per["k_quantize"]
-    per["k_quantize"] = full * (rows - rows // 2 // 64 * 64) // rows
-    per["k_quantize_lean"] = full - per["k_quantize"]
+    r_lean = (rows // 2 if normalisers_given else rows // 3) // 64 * 64
+    launches = LEAN_LAUNCHES[normalisers_given]
+    per["k_quantize"] = full * (rows - launches * r_lean) // rows
+    per["k_quantize_lean"] = full * r_lean // rows
     return per, path
+
+
+# k_quantize_lean launches per tp_evict call, without / with the normalisers given
+LEAN_LAUNCHES = {False: 2, True: 1}
 
 
 def source_sha256(kernel: str) -> str:
@@ -340,7 +353,7 @@ def main():
     stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
 
-    per, path_bytes = algorithmic_bytes(w, ko[-1], not args.no_full_codes)
+    per, path_bytes = algorithmic_bytes(w, ko[-1], not args.no_full_codes, lse is not None)
     # the two score passes are bf16 contractions (2 flop per guide-row x token x dim); the
     # other kernels stream HBM
     score_flops = 2 * w.L * w.Hq * sum(g * n for g, n in zip(w.guide_lens, w.ctx_lens)) * w.d
@@ -373,7 +386,7 @@ def main():
     if same_fmt and kg is None and lse is None and not args.no_full_codes:
         parts = [measured_traffic(kn, args.workload) for kn in STAGES + ["k_quantize_lean"]]
         if all(p is not None for p in parts):
-            tot = sum(parts)
+            tot = sum(parts) + (LEAN_LAUNCHES[False] - 1) * parts[-1]
             measured_path = {"achieved": round(tot / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": round(tot / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": tot}
     out = {

@@ -326,7 +326,7 @@ struct AuxStream {
   std::mutex enqueue;
   bool ready = false;
   hipStream_t stream = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr;
 };
 constexpr int kMaxDevices = 64;
 AuxStream g_aux[kMaxDevices];
@@ -346,6 +346,7 @@ tp_status aux_stream_for(hipStream_t st, AuxStream*& out) {
     // default priority (the caller's streams' priority is not inherited)
     if (e == hipSuccess && !a.stream) e = hipStreamCreateWithFlags(&a.stream, hipStreamNonBlocking);
     if (e == hipSuccess && !a.fork) e = hipEventCreateWithFlags(&a.fork, hipEventDisableTiming);
+    if (e == hipSuccess && !a.fork2) e = hipEventCreateWithFlags(&a.fork2, hipEventDisableTiming);
     if (e == hipSuccess && !a.join) e = hipEventCreateWithFlags(&a.join, hipEventDisableTiming);
     if (cur != dev) {
       const hipError_t e2 = hipSetDevice(cur);
@@ -536,41 +537,58 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   if (s != TP_OK) return s;
   std::lock_guard<std::mutex> lk(aux->enqueue);
 
-  // Step 2 is split in two halves of the V rows.  The first half is quantised by the lean
-  // kernel on the second stream, resident beside score pass 1 (whose workgroups leave one
-  // wave slot and 48 VGPRs per SIMD free) and using its idle memory bandwidth; the second by
-  // the regular kernel between the normalisers and score pass 2, which then starts after a
+  // Step 2 is split by rows of V, each row quantised once, by one of three launches with the
+  // same arithmetic.  The lean kernel, on the second stream, takes the first part while score
+  // pass 1 runs (its workgroups leave one wave slot and 48 VGPRs per SIMD free, and it uses
+  // HBM well below the copy rate) and the last part while pass 2 runs; the regular kernel
+  // takes the middle part between the normalisers and pass 2, which then starts after a
   // memory-bound kernel instead of right after pass 1, at a higher power-limited clock.
-  // Every row is quantised once, by one of the two, with the same arithmetic.
-  const int64_t r1 = qa.rows / 2 / 64 * 64;
-  tp::QuantArgs qa1 = qa, qa2 = qa;
-  qa1.rows = r1;
-  qa2.rows = qa.rows - r1;
-  qa2.v += r1 * dims->head_dim;
-  qa2.scales += r1;
-  if (qa2.vq) qa2.vq += r1 * (int64_t)row_bytes_of(qfmt, bits, dims->head_dim);
+  // With pass 1 each lean part is a third of the rows; with the normalisers given (no pass 1)
+  // the lean kernel takes the first half and nothing runs beside pass 2.  Parts are rounded
+  // down to 64 rows.
+  const bool pass1 = ga.lse_in == nullptr;
+  const int64_t r_lean = (pass1 ? qa.rows / 3 : qa.rows / 2) / 64 * 64;
+  const int64_t r_mid_end = pass1 ? qa.rows - r_lean : qa.rows;
+  const int64_t vrow = (int64_t)row_bytes_of(qfmt, bits, dims->head_dim);
+  auto part = [&](int64_t r0, int64_t r1) {
+    tp::QuantArgs p = qa;
+    p.rows = r1 - r0;
+    p.v += r0 * dims->head_dim;
+    p.scales += r0;
+    if (p.vq) p.vq += r0 * vrow;
+    return p;
+  };
+  const tp::QuantArgs qa1 = part(0, r_lean), qa2 = part(r_lean, r_mid_end), qa3 = part(r_mid_end, qa.rows);
   hipError_t e = hipSuccess;
   if (ev) e = hipEventRecord(ev[0], st);
   if (e == hipSuccess) e = hipEventRecord(aux->fork, st);
   if (e == hipSuccess) e = hipStreamWaitEvent(aux->stream, aux->fork, 0);
   if (e == hipSuccess) e = tp::launch_quantize_lean(qa1, dims->head_dim, aux->stream);
-  if (e == hipSuccess) e = hipEventRecord(aux->join, aux->stream);
+  // called by the score pass between the normalisers and pass 2 (exactly once on success)
   struct Mid {
-    const tp::QuantArgs* qa;
+    const tp::QuantArgs* mid;
+    const tp::QuantArgs* last;
     int head_dim;
     hipStream_t st;
     hipEvent_t done;
-  } mid{&qa2, dims->head_dim, st, ev ? ev[3] : nullptr};
+    AuxStream* aux;
+  } mid{&qa2, &qa3, dims->head_dim, st, ev ? ev[3] : nullptr, aux};
   auto quant_between = [](void* c) -> hipError_t {
     const Mid* m = (const Mid*)c;
-    hipError_t r = tp::launch_quantize(*m->qa, m->head_dim, m->st);
+    hipError_t r = tp::launch_quantize(*m->mid, m->head_dim, m->st);
     if (r == hipSuccess && m->done) r = hipEventRecord(m->done, m->st);
+    if (r == hipSuccess && m->last->rows > 0) {
+      r = hipEventRecord(m->aux->fork2, m->st);
+      if (r == hipSuccess) r = hipStreamWaitEvent(m->aux->stream, m->aux->fork2, 0);
+      if (r == hipSuccess) r = tp::launch_quantize_lean(*m->last, m->head_dim, m->aux->stream);
+    }
+    if (r == hipSuccess) r = hipEventRecord(m->aux->join, m->aux->stream);
     return r;
   };
   hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr, ev ? ev[5] : nullptr};
   if (e == hipSuccess)
     e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, quant_between, &mid);
-  // the selection reads the scales: wait for the lean kernel too
+  // the selection reads the scales: wait for the second stream's parts too
   if (e == hipSuccess) e = hipStreamWaitEvent(st, aux->join, 0);
   if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);

@@ -2,7 +2,7 @@
 path's bytes follow the compulsory-traffic formula per (layer, KV head, context token) at
 d = 128 — read K and V once, write the 8-bit codes and the fp32 scale (644 B), plus per
 kept token the re-read of its K row, codes and scale and the write of the compact cache and
-index (780 B) — and the per-kernel counts of step 2 add up over its two launches."""
+index (780 B) — and the per-launch counts of step 2 add up over its launches."""
 import os
 import sys
 
@@ -29,8 +29,16 @@ def test_path_bytes_128k():
     q_bytes = w.L * w.Hq * w.g_tot * w.d * 2
     assert path == LH * (644 * n + 780 * k) + q_bytes
     assert abs(path / 1e9 - 24.24) < 0.01
-    # step 2's two launches (the second-stream half and the rest) cover every V row once
-    assert per["k_quantize"] + per["k_quantize_lean"] == LH * n * (2 * w.d + w.d + 4)
+    # step 2's launches (a third of the rows beside each score pass on the second stream, the
+    # rest between the passes) cover every V row once
+    row = 2 * w.d + w.d + 4
+    assert per["k_quantize"] + 2 * per["k_quantize_lean"] == LH * n * row
+    assert per["k_quantize_lean"] == (LH * n // 3 // 64 * 64) * row
+    # with the normalisers given: the first half on the second stream, the rest between
+    per_g, _ = bench.algorithmic_bytes(w, k, normalisers_given=True)
+    assert per_g["k_quantize"] + per_g["k_quantize_lean"] == LH * n * row
+    assert per_g["k_quantize_lean"] == (LH * n // 2 // 64 * 64) * row
+    assert bench.LEAN_LAUNCHES == {False: 2, True: 1}
 
 
 def test_path_bytes_scales_only_and_int4():

@@ -1,7 +1,7 @@
 """Resource budgets the kernels rely on, checked on the compiled code (CPU only: hipcc
-cross-compiles for gfx950).  tp_evict runs the lean quantisation beside score pass 1: one
-pass-1 workgroup (8 waves, two per SIMD) and one lean workgroup (4 waves, one per SIMD) must
-fit one CU together, in VGPRs (512 per SIMD lane, allocated in granules of 8) and LDS
+cross-compiles for gfx950).  tp_evict runs the lean quantisation beside each score pass: one
+score-pass workgroup (8 waves, two per SIMD) and one lean workgroup (4 waves, one per SIMD)
+must fit one CU together, in VGPRs (512 per SIMD lane, allocated in granules of 8) and LDS
 (160 KB); otherwise the lean kernel waits for free CUs and the overlap is lost."""
 import os
 import re
@@ -51,8 +51,9 @@ def kernels():
     return res
 
 
-def test_lean_quantisation_fits_beside_score_pass_1(kernels):
-    passes = {n: v for n, v in kernels.items() if "k_guide_stats" in n}
+@pytest.mark.parametrize("kernel", ["k_guide_stats", "k_guide_attn"])
+def test_lean_quantisation_fits_beside_score_passes(kernels, kernel):
+    passes = {n: v for n, v in kernels.items() if kernel in n}
     leans = {n: v for n, v in kernels.items() if "k_quantize_lean" in n}
     assert passes and leans
     for pn, (pv, plds) in passes.items():

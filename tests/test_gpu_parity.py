@@ -478,8 +478,8 @@ def test_evict_matches_the_four_calls(gpu_lib):
               W.ragged8().with_(name="ragged-fp8", L=2, ctx_lens=(9000, 1, 8193), guide_lens=(32, 128, 7),
                                 keep_budget=500, qfmt=1),
               W.llama8b_32k().with_(name="two-row-groups", L=1, ctx_lens=(5000,), guide_lens=(100,)),
-              # fewer than 128 V rows (the second stream's half is empty), and a half that is
-              # not a whole number of 64-row groups
+              # fewer than 192 V rows (the second stream's parts are empty), and a middle part
+              # that is not a whole number of 64-row groups
               W.tiny().with_(name="tiny-61-rows", Hq=2, Hkv=1, ctx_lens=(1, 60), guide_lens=(3, 2)),
               W.tiny().with_(name="tiny-401-rows", Hq=4, Hkv=1, ctx_lens=(333, 68), guide_lens=(5, 7))):
         pu.log(f"tp_evict vs four calls: {w.describe()}")
