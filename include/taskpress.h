@@ -22,7 +22,7 @@
  *  - Ownership: the caller allocates every input, output and workspace buffer.
  *    The library allocates no memory and keeps no pointer after returning; buffers
  *    must stay valid until the enqueued work has completed.  (tp_evict keeps one
- *    stream and two events of its own per device: see tp_evict.)
+ *    stream and three events of its own per device: see tp_evict.)
  *  - Execution is asynchronous and stream-ordered; nothing synchronises inside a
  *    call.  Calls are re-entrant.  Results are bit-identical from run to run (no
  *    floating-point atomics; fixed reduction orders).
@@ -256,9 +256,10 @@ typedef struct tp_profile {
  * and the codes of the evicted rows are never written.
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
  * pass's workspace followed by the selection's).
- * Step 2 of the first half of the V rows runs on a second stream of the library's,
- * concurrently with score pass 1 (same arithmetic, so the results are as for the separate
- * calls).  That stream and two events are created, with default priority, by the first
+ * Step 2 of two thirds of the V rows runs on a second stream of the library's, a third
+ * concurrently with each score pass (with guide_lse given: the first half, concurrently
+ * with the rest of the step); the arithmetic is the same, so the results are as for the
+ * separate calls.  That stream and three events are created, with default priority, by the first
  * tp_evict call on a device and kept until the process ends (TP_ERR_HIP if that fails); the
  * work is forked from and joined back to `stream`, so the call stays stream-ordered and may
  * be captured into a graph (once the first call on the device, which creates the stream,
