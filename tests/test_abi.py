@@ -257,3 +257,11 @@ def test_evict_workspace_size():
     assert B.tp_workspace_size(B.TP_FN_EVICT, d, bt) == g + s
     with pytest.raises(B.TaskPressError):
         B.tp_workspace_size(B.TP_FN_EVICT, d, B.Batch([0, 131072]))
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    """Without the built library the binding raises instead of falling back to anything."""
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", os.path.join(ROOT, "no-such-dir", "libtaskpress.so"))
+    with pytest.raises(ImportError, match="is missing"):
+        B.load()
