@@ -294,8 +294,9 @@ def main():
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the path shards by "
-              f"(layer, KV head, sequence) with no communication, see the design notes.", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); the path shards by "
+              f"(layer, KV head, sequence) with no communication, so each GPU would run it on its own share.",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
