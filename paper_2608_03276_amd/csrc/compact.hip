@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_quant(CompactArgs a
   const int64_t r0 = (int64_t)blockIdx.x * RPB * kRowsPerLane + threadIdx.x / LPR;
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
-  build_tables(tab, a.qmax);
+  build_tables<K == kQInt8>(tab, a.qmax);
   __syncthreads();
   int64_t src[kRowsPerLane];
   bool ok[kRowsPerLane];
@@ -122,11 +122,13 @@ hipError_t launch_compact(const CompactArgs& a, int segments, int head_dim, hipS
     const int kind = qkind_of(a.qfmt, a.bits);
 #define TP_COMPACT_QUANT(D_, K_) hipLaunchKernelGGL((k_compact_quant<D_, K_>), grid, dim3(kCompactThreads), 0, stream, a)
     if (head_dim == 128) {
-      if (kind == kQByte) TP_COMPACT_QUANT(128, kQByte);
+      if (kind == kQInt8) TP_COMPACT_QUANT(128, kQInt8);
+      else if (kind == kQByte) TP_COMPACT_QUANT(128, kQByte);
       else if (kind == kQNibble) TP_COMPACT_QUANT(128, kQNibble);
       else TP_COMPACT_QUANT(128, kQE4M3);
     } else {
-      if (kind == kQByte) TP_COMPACT_QUANT(64, kQByte);
+      if (kind == kQInt8) TP_COMPACT_QUANT(64, kQInt8);
+      else if (kind == kQByte) TP_COMPACT_QUANT(64, kQByte);
       else if (kind == kQNibble) TP_COMPACT_QUANT(64, kQNibble);
       else TP_COMPACT_QUANT(64, kQE4M3);
     }

@@ -14,7 +14,11 @@
 // significand that the workgroup computes with IEEE divisions.  The quotient is
 // q0 = v * y' corrected once, fl(q0 + fma(-q0, gamma, v) * y'), and the integer code is the
 // low bits of that value plus 1.5 * 2^23 (an RNE round to an integer whose two's complement
-// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  An E4M3
+// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  For int8
+// (qmax = 127) the table holds instead the multipliers of int8_recip_table.h, each within one
+// ulp of 1/fl32(m/127) and chosen so that a single fma(v, y', 1.5 * 2^23), one
+// rounding of the exact product, gives every code of that significand (checked exhaustively
+// by the generator); no correction step is needed there.  An E4M3
 // code is the hardware conversion of that value clamped to +-448 (it can exceed 448 by an
 // ulp), with the sign of v.  Every intermediate that can decide a code is a normal number
 // in this range, and an exhaustive check over every (A, v) pair of bf16 values, both signs,
@@ -29,6 +33,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "int8_recip_table.h"
 #include "taskpress.h"
 
 namespace tp {
@@ -39,26 +44,33 @@ struct QuantFmt {
   float qmax;
 };
 
-// Code formats, fixed per kernel instance: one integer code per byte (b in [5, 8]), two per
-// byte (b <= 4), or E4M3.
-enum QKind { kQByte = 0, kQNibble = 1, kQE4M3 = 2 };
+// Code formats, fixed per kernel instance: one integer code per byte (b in [5, 7]; int8 has
+// its own instance for its single-rounding path), two per byte (b <= 4), or E4M3.
+enum QKind { kQByte = 0, kQNibble = 1, kQE4M3 = 2, kQInt8 = 3 };
 
 __host__ __device__ inline int qkind_of(int32_t qfmt, int32_t bits) {
-  return qfmt == TP_QFMT_INT ? (bits <= 4 ? kQNibble : kQByte) : kQE4M3;
+  if (qfmt != TP_QFMT_INT) return kQE4M3;
+  return bits <= 4 ? kQNibble : (bits == 8 ? kQInt8 : kQByte);
 }
 
 // gamma and 1/gamma of the significand m = 1 + t/128 of an absmax, for the common path.
 struct QuantTables {
   float g[128];  // fl32(m / qmax)
-  float y[128];  // fl32(1 / g)
+  float y[128];  // fl32(1 / g), or for qmax = 127 the single-rounding multiplier
 };
 
 // All threads of the block call this, followed by a barrier before the first quant_piece.
+// INT8: the kernel instance of the int8 format (qmax = 127), whose y are the single-rounding
+// multipliers.
+template <bool INT8>
 __device__ inline void build_tables(QuantTables& tab, float qmax) {
   for (int t = threadIdx.x; t < 128; t += blockDim.x) {
     const float g = (1.0f + (float)t * 0.0078125f) / qmax;
     tab.g[t] = g;
-    tab.y[t] = 1.0f / g;
+    uint32_t y = __float_as_uint(1.0f / g);
+    if (INT8)
+      y = y + (uint32_t)((kInt8RecipUp[t >> 6] >> (t & 63)) & 1u) - (uint32_t)((kInt8RecipDown[t >> 6] >> (t & 63)) & 1u);
+    tab.y[t] = __uint_as_float(y);
   }
 }
 
@@ -165,6 +177,16 @@ __device__ inline void codes_fast(const uint32_t (&w)[4], float gamma, float ys,
   }
 }
 
+// int8 codes of 8 values on the common path: one rounding of the exact v * y' to the integer
+// grid, whose two's complement sits in the low bits of the result.
+__device__ inline void codes_fast_int8(const uint32_t (&w)[4], float ys, uint32_t (&code)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    code[i] = __float_as_uint(fmaf(__uint_as_float(h), ys, kRoundMagic));
+  }
+}
+
 // E4M3 codes of 8 values on the common path, packed: the corrected quotient, clamped to
 // +-448 (it can exceed 448 by an ulp), with the sign of v (so -0 keeps its sign), converted
 // two at a time by the hardware fp32 -> OCP E4M3 conversion (nearest, ties to even,
@@ -205,7 +227,10 @@ __device__ inline float quant_piece(const uint4& x, const QuantTables& tab, cons
       out = codes_fast_e4m3(w, gamma, ys);
       return gamma;
     }
-    codes_fast<K>(w, gamma, ys, code);
+    if (K == kQInt8)
+      codes_fast_int8(w, ys, code);
+    else
+      codes_fast<K>(w, gamma, ys, code);
   } else {
     const float amax = __uint_as_float(mx << 16);
     gamma = amax / f.qmax;

@@ -26,7 +26,7 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
   if (K != kScalesOnly) {
-    build_tables(tab, a.qmax);
+    build_tables<K == kQInt8>(tab, a.qmax);
     __syncthreads();
   }
 
@@ -67,6 +67,9 @@ void launch_d(const QuantArgs& a, unsigned blocks, hipStream_t stream) {
     return;
   }
   switch (qkind_of(a.qfmt, a.bits)) {
+    case kQInt8:
+      hipLaunchKernelGGL((k_quantize<D, kQInt8>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
+      break;
     case kQByte:
       hipLaunchKernelGGL((k_quantize<D, kQByte>), dim3(blocks), dim3(kQuantThreads), 0, stream, a);
       break;
@@ -99,7 +102,7 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_lean(QuantArgs a) {
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
   if (K != kScalesOnly) {
-    build_tables(tab, a.qmax);
+    build_tables<K == kQInt8>(tab, a.qmax);
     __syncthreads();
   }
   const int64_t stride = (int64_t)gridDim.x * kWaves * kLeanLoads * RPW;
@@ -141,6 +144,9 @@ void launch_lean_d(const QuantArgs& a, hipStream_t stream) {
     return;
   }
   switch (qkind_of(a.qfmt, a.bits)) {
+    case kQInt8:
+      hipLaunchKernelGGL((k_quantize_lean<D, kQInt8>), grid, block, 0, stream, a);
+      break;
     case kQByte:
       hipLaunchKernelGGL((k_quantize_lean<D, kQByte>), grid, block, 0, stream, a);
       break;
