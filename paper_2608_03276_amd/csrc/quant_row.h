@@ -148,8 +148,17 @@ __device__ inline void codes_divided(const uint32_t (&w)[4], float gamma, const 
 
 // Magnitude bits of the absmax of the row whose LPT pieces sit in LPT consecutive lanes (all
 // lanes call together): an integer max of the bf16 magnitudes, reduced across the lanes.
-template <int LPT>
+// PACKED: two magnitudes per packed 16-bit max (fewer vector instructions beside the codes'
+// arithmetic); the scales-only kernel keeps the 32-bit form, which measured faster there.
+template <int LPT, bool PACKED = true>
 __device__ inline uint32_t row_absmax_bits(const uint32_t (&w)[4]) {
+  if (PACKED) {
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    u16x2 m2 = {0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, w[i] & 0x7FFF7FFFu));
+    return group_max<LPT>(max((uint32_t)m2.x, (uint32_t)m2.y));
+  }
   uint32_t mx = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) mx = max(mx, max(w[i] & 0x7FFFu, (w[i] >> 16) & 0x7FFFu));
@@ -160,7 +169,7 @@ __device__ inline uint32_t row_absmax_bits(const uint32_t (&w)[4]) {
 template <int LPT>
 __device__ inline float scale_piece(const uint4& x, const QuantFmt& f) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  return __uint_as_float(row_absmax_bits<LPT>(w) << 16) / f.qmax;
+  return __uint_as_float(row_absmax_bits<LPT, false>(w) << 16) / f.qmax;
 }
 
 // Codes of 8 values on the common path: y = v / gamma corrected as above; an integer code is
