@@ -543,11 +543,11 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   // HBM well below the copy rate) and the last part while pass 2 runs; the regular kernel
   // takes the middle part between the normalisers and pass 2, which then starts after a
   // memory-bound kernel instead of right after pass 1, at a higher power-limited clock.
-  // With pass 1 each lean part is a third of the rows; with the normalisers given (no pass 1)
-  // the lean kernel takes the first half and nothing runs beside pass 2.  Parts are rounded
-  // down to 64 rows.
+  // With pass 1 each lean part is 2/5 of the rows (the middle fifth runs alone); with the
+  // normalisers given (no pass 1) the lean kernel takes the first half and nothing runs
+  // beside pass 2.  Parts are rounded down to 64 rows.
   const bool pass1 = ga.lse_in == nullptr;
-  const int64_t r_lean = (pass1 ? qa.rows / 3 : qa.rows / 2) / 64 * 64;
+  const int64_t r_lean = (pass1 ? qa.rows * 2 / 5 : qa.rows / 2) / 64 * 64;
   const int64_t r_mid_end = pass1 ? qa.rows - r_lean : qa.rows;
   const int64_t vrow = (int64_t)row_bytes_of(qfmt, bits, dims->head_dim);
   auto part = [&](int64_t r0, int64_t r1) {

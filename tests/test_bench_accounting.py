@@ -29,11 +29,11 @@ def test_path_bytes_128k():
     q_bytes = w.L * w.Hq * w.g_tot * w.d * 2
     assert path == LH * (644 * n + 780 * k) + q_bytes
     assert abs(path / 1e9 - 24.24) < 0.01
-    # step 2's launches (a third of the rows beside each score pass on the second stream, the
-    # rest between the passes) cover every V row once
+    # step 2's launches (2/5 of the rows beside each score pass on the second stream, the rest
+    # between the passes) cover every V row once
     row = 2 * w.d + w.d + 4
     assert per["k_quantize"] + 2 * per["k_quantize_lean"] == LH * n * row
-    assert per["k_quantize_lean"] == (LH * n // 3 // 64 * 64) * row
+    assert per["k_quantize_lean"] == (LH * n * 2 // 5 // 64 * 64) * row
     # with the normalisers given: the first half on the second stream, the rest between
     per_g, _ = bench.algorithmic_bytes(w, k, normalisers_given=True)
     assert per_g["k_quantize"] + per_g["k_quantize_lean"] == LH * n * row
