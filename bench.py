@@ -28,11 +28,11 @@ KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
                   "k_guide_attn": ["guide_scores.hip", "tp_internal.h"],
                   "k_guide_pool": ["guide_scores.hip", "tp_internal.h"],
                   # the rows each step-2 launch takes are set by tp_evict
-                  "k_quantize": ["quantize.hip", "quant_row.h", "int8_recip_table.h", "tp_internal.h", "abi.cpp"],
-                  "k_quantize_lean": ["quantize.hip", "quant_row.h", "int8_recip_table.h", "tp_internal.h", "abi.cpp"],
+                  "k_quantize": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
+                  "k_quantize_lean": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
                   "k_select": ["select.hip", "tp_internal.h"],
                   "k_compact": ["compact.hip", "tp_internal.h"],
-                  "k_compact_quant": ["compact.hip", "quant_row.h", "int8_recip_table.h", "tp_internal.h"],
+                  "k_compact_quant": ["compact.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h"],
                   "k_lse_import": ["guide_scores.hip", "tp_internal.h"]}
 
 
@@ -89,7 +89,10 @@ def source_sha256(kernel: str) -> str:
 
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_2608_03276_amd", "csrc", name), "rb") as f:
+        path = os.path.join(ROOT, "paper_2608_03276_amd", "csrc", name)
+        if not os.path.exists(path):  # a listed source that is gone: no summary can match
+            return "missing:" + name
+        with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 

@@ -196,6 +196,7 @@ tp_status prepare_quant(const tp_dims* dims, const tp_batch* batch, const void* 
   a.qfmt = qfmt;
   a.bits = bits;
   a.qmax = qmax_of(qfmt, bits);
+  a.ro = tp::recip_offsets_for(a.qmax);
   return TP_OK;
 }
 
@@ -287,6 +288,7 @@ tp_status prepare_compact(const tp_dims* dims, const tp_batch* batch, const int6
   a.qfmt = qfmt;
   a.bits = bits;
   a.qmax = qmax_of(qfmt, bits);
+  a.ro = tp::recip_offsets_for(a.qmax);
   a.bt = batch_args(batch, false);
   return TP_OK;
 }

@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_quant(CompactArgs a
   const int64_t r0 = (int64_t)blockIdx.x * RPB * kRowsPerLane + threadIdx.x / LPR;
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
-  build_tables<K == kQInt8>(tab, a.qmax);
+  build_tables(tab, a.qmax, a.ro.off);
   __syncthreads();
   int64_t src[kRowsPerLane];
   bool ok[kRowsPerLane];

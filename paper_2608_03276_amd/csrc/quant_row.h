@@ -14,11 +14,13 @@
 // significand that the workgroup computes with IEEE divisions.  The quotient is
 // q0 = v * y' corrected once, fl(q0 + fma(-q0, gamma, v) * y'), and the integer code is the
 // low bits of that value plus 1.5 * 2^23 (an RNE round to an integer whose two's complement
-// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  For int8
-// (qmax = 127) the table holds instead the multipliers of int8_recip_table.h, each within one
-// ulp of 1/fl32(m/127) and chosen so that a single fma(v, y', 1.5 * 2^23), one
-// rounding of the exact product, gives every code of that significand (checked exhaustively
-// by the generator); no correction step is needed there.  An E4M3
+// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  Most
+// significands do not need the correction: quant_recip_table.h marks, per format, a
+// multiplier y'' within one ulp of 1/fl32(m/qmax) for which one multiply gives every code of
+// that significand (checked exhaustively by its generator): for int8 fma(v, y'', 1.5 * 2^23),
+// a single rounding of the exact product onto the integer grid; for the other integers
+// fl32(v * y'') + 1.5 * 2^23; for E4M3 the code of fl32(v * y'').  A wave takes that path
+// when every row in it has such a multiplier (int8: always), else the corrected one.  An E4M3
 // code is the hardware conversion of that value clamped to +-448 (it can exceed 448 by an
 // ulp), with the sign of v.  Every intermediate that can decide a code is a normal number
 // in this range, and an exhaustive check over every (A, v) pair of bf16 values, both signs,
@@ -33,8 +35,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "int8_recip_table.h"
 #include "taskpress.h"
+#include "tp_internal.h"
 
 namespace tp {
 
@@ -55,22 +57,21 @@ __host__ __device__ inline int qkind_of(int32_t qfmt, int32_t bits) {
 
 // gamma and 1/gamma of the significand m = 1 + t/128 of an absmax, for the common path.
 struct QuantTables {
-  float g[128];  // fl32(m / qmax)
-  float y[128];  // fl32(1 / g), or for qmax = 127 the single-rounding multiplier
+  float g[128];   // fl32(m / qmax)
+  float y[128];   // fl32(1 / g)
+  float ym[128];  // the one-multiply multiplier y'', or -1 where the significand has none
 };
 
 // All threads of the block call this, followed by a barrier before the first quant_piece.
-// INT8: the kernel instance of the int8 format (qmax = 127), whose y are the single-rounding
-// multipliers.
-template <bool INT8>
-__device__ inline void build_tables(QuantTables& tab, float qmax) {
+// off: the ulp offsets of the one-multiply multipliers (recip_offsets_for(qmax)).
+__device__ inline void build_tables(QuantTables& tab, float qmax, const int8_t* off) {
   for (int t = threadIdx.x; t < 128; t += blockDim.x) {
     const float g = (1.0f + (float)t * 0.0078125f) / qmax;
+    const uint32_t y = __float_as_uint(1.0f / g);
+    const int o = off[t];
     tab.g[t] = g;
-    uint32_t y = __float_as_uint(1.0f / g);
-    if (INT8)
-      y = y + (uint32_t)((kInt8RecipUp[t >> 6] >> (t & 63)) & 1u) - (uint32_t)((kInt8RecipDown[t >> 6] >> (t & 63)) & 1u);
     tab.y[t] = __uint_as_float(y);
+    tab.ym[t] = o == kNoMultiplier ? -1.0f : __uint_as_float(y + (uint32_t)o);
   }
 }
 
@@ -186,13 +187,26 @@ __device__ inline void codes_fast(const uint32_t (&w)[4], float gamma, float ys,
   }
 }
 
-// int8 codes of 8 values on the common path: one rounding of the exact v * y' to the integer
+// int8 codes of 8 values on the common path: one rounding of the exact v * y'' to the integer
 // grid, whose two's complement sits in the low bits of the result.
 __device__ inline void codes_fast_int8(const uint32_t (&w)[4], float ys, uint32_t (&code)[8]) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
     code[i] = __float_as_uint(fmaf(__uint_as_float(h), ys, kRoundMagic));
+  }
+}
+
+// Other integer codes with a one-multiply multiplier: the product rounded to fp32, then to an
+// integer by the add (two roundings, exactly as the table was checked; the multiply and the
+// add must not be fused).
+__device__ inline void codes_mul(const uint32_t (&w)[4], float ys, uint32_t (&code)[8]) {
+#pragma clang fp contract(off)
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float q = __uint_as_float(h) * ys;
+    code[i] = __float_as_uint(q + kRoundMagic);
   }
 }
 
@@ -217,6 +231,22 @@ __device__ inline uint2 codes_fast_e4m3(const uint32_t (&w)[4], float gamma, flo
   return make_uint2(lo, hi);
 }
 
+// E4M3 codes of 8 values with a one-multiply multiplier, packed as codes_fast_e4m3.
+__device__ inline uint2 codes_mul_e4m3(const uint32_t (&w)[4], float ys) {
+  float y[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16);
+    const float v = __uint_as_float(h);
+    y[i] = __builtin_copysignf(__builtin_amdgcn_fmed3f(v * ys, -448.0f, 448.0f), v);
+  }
+  uint32_t lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+  lo = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], (int)lo, true);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[4], y[5], 0, false);
+  hi = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[6], y[7], (int)hi, true);
+  return make_uint2(lo, hi);
+}
+
 // Quantise the lane's 16-byte piece `x` (8 bf16 values) of a row whose LPT pieces sit in
 // LPT consecutive lanes; every lane of the wave must call this together (the absmax is
 // reduced across lanes, and the path is chosen per wave).  Returns gamma (the same on all
@@ -231,15 +261,24 @@ __device__ inline float quant_piece(const uint4& x, const QuantTables& tab, cons
   if (__builtin_amdgcn_ballot_w64(ef < kFastExpLo || ef > kFastExpHi) == 0) {
     const int t = (int)(mx & 0x7Fu);
     gamma = __builtin_amdgcn_ldexpf(tab.g[t], ef - 127);
-    const float ys = __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef);
-    if (K == kQE4M3) {
-      out = codes_fast_e4m3(w, gamma, ys);
-      return gamma;
-    }
-    if (K == kQInt8)
-      codes_fast_int8(w, ys, code);
-    else
+    const float ym = tab.ym[t];
+    if (K == kQInt8) {  // every int8 significand has a multiplier
+      codes_fast_int8(w, __builtin_amdgcn_ldexpf(ym, 127 - ef), code);
+    } else if (__builtin_amdgcn_ballot_w64(!(ym > 0.0f)) == 0) {
+      const float ys = __builtin_amdgcn_ldexpf(ym, 127 - ef);
+      if (K == kQE4M3) {
+        out = codes_mul_e4m3(w, ys);
+        return gamma;
+      }
+      codes_mul(w, ys, code);
+    } else {
+      const float ys = __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef);
+      if (K == kQE4M3) {
+        out = codes_fast_e4m3(w, gamma, ys);
+        return gamma;
+      }
       codes_fast<K>(w, gamma, ys, code);
+    }
   } else {
     const float amax = __uint_as_float(mx << 16);
     gamma = amax / f.qmax;

@@ -26,7 +26,7 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize(QuantArgs a) {
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
   if (K != kScalesOnly) {
-    build_tables<K == kQInt8>(tab, a.qmax);
+    build_tables(tab, a.qmax, a.ro.off);
     __syncthreads();
   }
 
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kQuantThreads) void k_quantize_lean(QuantArgs a) {
   const QuantFmt f{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   __shared__ QuantTables tab;
   if (K != kScalesOnly) {
-    build_tables<K == kQInt8>(tab, a.qmax);
+    build_tables(tab, a.qmax, a.ro.off);
     __syncthreads();
   }
   const int64_t stride = (int64_t)gridDim.x * kWaves * kLeanLoads * RPW;

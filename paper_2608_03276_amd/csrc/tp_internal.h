@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "quant_recip_table.h"
 #include "taskpress.h"
 
 namespace tp {
@@ -71,6 +72,28 @@ hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t str
                                GuideBetween between = nullptr, void* ctx = nullptr);
 
 // ---------------------------------------------------------------- step 2 (V scales)
+// The one-multiply multipliers of the format with this qmax, per absmax significand t: the
+// ulp offset from fl32(1/fl32(m/qmax)) (-1, 0, 1), or kNoMultiplier where there is none (also
+// for every t of a qmax the table does not hold, which keeps the corrected quotient).
+constexpr int8_t kNoMultiplier = 2;
+struct RecipOffsets {
+  int8_t off[128];
+};
+inline RecipOffsets recip_offsets_for(float qmax) {
+  RecipOffsets r;
+  const RecipMasks* m = nullptr;
+  for (int f = 0; f < 8; ++f)
+    if (kRecipQmax[f] == qmax) m = &kRecipMasks[f];
+  for (int t = 0; t < 128; ++t) {
+    const int w = t >> 6, b = t & 63;
+    if (m == nullptr || ((m->none[w] >> b) & 1u))
+      r.off[t] = kNoMultiplier;
+    else
+      r.off[t] = (int8_t)(((m->up[w] >> b) & 1u) ? 1 : ((m->down[w] >> b) & 1u) ? -1 : 0);
+  }
+  return r;
+}
+
 struct QuantArgs {
   const uint16_t* v;  // bf16 [rows][d]
   float* scales;      // fp32 [rows]
@@ -78,6 +101,7 @@ struct QuantArgs {
   int64_t rows;       // L * Hkv * N_tot
   int32_t qfmt, bits;
   float qmax;
+  RecipOffsets ro;    // recip_offsets_for(qmax)
 };
 hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream);
 
@@ -115,6 +139,7 @@ struct CompactArgs {
   int32_t row_bytes;
   int32_t qfmt, bits;  // format of the codes when v is set
   float qmax;
+  RecipOffsets ro;     // recip_offsets_for(qmax)
   int64_t kept_off[TP_MAX_BATCH + 1];
   BatchArgs bt;
 };

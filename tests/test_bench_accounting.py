@@ -52,3 +52,11 @@ def test_path_bytes_scales_only_and_int4():
     w4 = w.with_(bits=4)
     _, path4 = bench.algorithmic_bytes(w4, k)
     assert path4 == LH * ((256 + 256 + 64 + 4) * n + k * (2 * (256 + 64 + 4) + 4)) + q_bytes
+
+
+def test_kernel_source_lists_name_existing_files():
+    """Every source a traffic summary is keyed on exists (a renamed file would otherwise leave
+    every summary stale without notice)."""
+    for kernel, names in bench.KERNEL_SOURCES.items():
+        for name in names:
+            assert os.path.exists(os.path.join(ROOT, "paper_2608_03276_amd", "csrc", name)), (kernel, name)
