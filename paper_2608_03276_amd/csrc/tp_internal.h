@@ -107,7 +107,7 @@ hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream)
 
 // The same quantisation in a form that stays resident beside a score-pass workgroup (one
 // workgroup per CU, one wave per SIMD, at most 48 VGPRs), for running part of step 2 on a
-// second stream concurrently with score pass 1.
+// second stream concurrently with the score passes.
 hipError_t launch_quantize_lean(const QuantArgs& a, int head_dim, hipStream_t stream);
 
 // ---------------------------------------------------------------- step 3 (select)
