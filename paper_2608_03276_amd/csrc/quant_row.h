@@ -9,23 +9,23 @@
 // with DPP row operations.
 //
 // Common path (every row of the wave has an absmax A in [2^-50, 2^114)): with A = m * 2^E,
-// m the bf16 significand, gamma = fl32(m/qmax) * 2^E and y' = fl32(1/fl32(m/qmax)) * 2^-E
-// exactly (power-of-two scalings of normal numbers), both read from a 128-entry table per
-// significand that the workgroup computes with IEEE divisions.  The quotient is
-// q0 = v * y' corrected once, fl(q0 + fma(-q0, gamma, v) * y'), and the integer code is the
-// low bits of that value plus 1.5 * 2^23 (an RNE round to an integer whose two's complement
-// sits in the low mantissa bits); no clamp is needed since |v/gamma| < qmax + 1/2.  Most
-// significands do not need the correction: quant_recip_table.h marks, per format, a
-// multiplier y'' within one ulp of 1/fl32(m/qmax) for which one multiply gives every code of
-// that significand (checked exhaustively by its generator): for int8 fma(v, y'', 1.5 * 2^23),
-// a single rounding of the exact product onto the integer grid; for the other integers
-// fl32(v * y'') + 1.5 * 2^23; for E4M3 the code of fl32(v * y'').  A wave takes that path
-// when every row in it has such a multiplier (int8: always), else the corrected one.  An E4M3
-// code is the hardware conversion of that value clamped to +-448 (it can exceed 448 by an
-// ulp), with the sign of v.  Every intermediate that can decide a code is a normal number
-// in this range, and an exhaustive check over every (A, v) pair of bf16 values, both signs,
-// for every qmax of the supported formats, gives the codes of the correctly rounded
-// quotient.
+// m the bf16 significand, gamma = fl32(m/qmax) * 2^E and y = fl32(1/fl32(m/qmax)) * 2^-E
+// exactly (power-of-two scalings of normal numbers), both read from 128-entry tables per
+// significand that the workgroup computes with IEEE divisions.
+//  - One multiply, where the significand has a checked multiplier: quant_recip_table.h
+//    marks, per format, a y'' within one ulp of 1/fl32(m/qmax) for which one multiply gives
+//    every code of that significand (its generator checks every bf16 v, both signs).  int8:
+//    fma(v, y'', 1.5 * 2^23), a single rounding of the exact product onto the integer grid,
+//    whose two's complement sits in the low mantissa bits (every int8 significand has one);
+//    other integers: fl32(v * y'') + 1.5 * 2^23; E4M3: the value fl32(v * y'').  A wave
+//    takes this path when every row in it has such a multiplier.
+//  - Corrected quotient otherwise: q0 = v * y, then fl(q0 + fma(-q0, gamma, v) * y), plus
+//    1.5 * 2^23 for an integer code; an exhaustive check over every (A, v) pair of bf16
+//    values, both signs, for every qmax of the supported formats, gives the codes of the
+//    correctly rounded quotient.
+// No clamp is needed for integer codes since |v/gamma| < qmax + 1/2.  An E4M3 code is the
+// hardware conversion of the value clamped to +-448 (it can exceed 448 by an ulp), with the
+// sign of v.  Every intermediate that can decide a code is a normal number in this range.
 // Other rows (tiny, zero or huge absmax) take the general path: the row is rescaled by
 // 2^-e (e = exponent of the absmax), the same corrected quotient is formed against
 // gamma' = gamma * 2^-e with one division per row, and the code is rounded and clamped
