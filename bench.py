@@ -67,21 +67,24 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True, normalisers_given
     if not full_codes:
         per["k_quantize"] = LH * n * (2 * d + 4)                        # read V, write scales
         path = LH * (n * (2 * d + 2 * d + 4) + kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4)) + q_bytes
-    # tp_evict quantises 2/5 of the V rows (rounded down to 64 rows) on its second stream beside
-    # each score pass (two k_quantize_lean launches), or, with the normalisers given, the first
-    # half beside nothing but the rest of the step (one launch); the k_quantize launch timed
-    # between the events does the rest
+    # tp_evict quantises a part of the V rows (rounded down to 64 rows) on its second stream
+    # beside each score pass (two k_quantize_lean launches), or, with the normalisers given,
+    # one part beside the rest of the step (one launch); the k_quantize launch timed between
+    # the events does the rest.  LEAN_PART gives the part as a fraction of the rows.
     rows = LH * n
     full = per["k_quantize"]
-    r_lean = (rows // 2 if normalisers_given else rows * 2 // 5) // 64 * 64
+    num, den = LEAN_PART[(normalisers_given, full_codes)]
+    r_lean = rows * num // den // 64 * 64
     launches = LEAN_LAUNCHES[normalisers_given]
     per["k_quantize"] = full * (rows - launches * r_lean) // rows
     per["k_quantize_lean"] = full * r_lean // rows
     return per, path
 
 
-# k_quantize_lean launches per tp_evict call, without / with the normalisers given
+# k_quantize_lean launches per tp_evict call, without / with the normalisers given, and the
+# rows of each launch as a fraction of all rows, by (normalisers given, full codes)
 LEAN_LAUNCHES = {False: 2, True: 1}
+LEAN_PART = {(False, True): (2, 5), (False, False): (1, 2), (True, True): (1, 2), (True, False): (3, 5)}
 
 
 def source_sha256(kernel: str) -> str:

@@ -256,9 +256,10 @@ typedef struct tp_profile {
  * and the codes of the evicted rows are never written.
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
  * pass's workspace followed by the selection's).
- * Step 2 of 4/5 of the V rows runs on a second stream of the library's, 2/5 concurrently
- * with each score pass (with guide_lse given: the first half, concurrently with the rest of
- * the step); the arithmetic is the same, so the results are as for the separate calls.  That stream and three events are created, with default priority, by the first
+ * Step 2 of most V rows runs on a second stream of the library's: 2/5 concurrently with each
+ * score pass (half with each when v_q is NULL), or, with guide_lse given, the first half
+ * (3/5 when v_q is NULL) concurrently with the rest of the step; the arithmetic is the same,
+ * so the results are as for the separate calls.  That stream and three events are created, with default priority, by the first
  * tp_evict call on a device and kept until the process ends (TP_ERR_HIP if that fails); the
  * work is forked from and joined back to `stream`, so the call stays stream-ordered and may
  * be captured into a graph (once the first call on the device, which creates the stream,

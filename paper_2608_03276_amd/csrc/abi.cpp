@@ -545,11 +545,14 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   // HBM well below the copy rate) and the last part while pass 2 runs; the regular kernel
   // takes the middle part between the normalisers and pass 2, which then starts after a
   // memory-bound kernel instead of right after pass 1, at a higher power-limited clock.
-  // With pass 1 each lean part is 2/5 of the rows (the middle fifth runs alone); with the
-  // normalisers given (no pass 1) the lean kernel takes the first half and nothing runs
-  // beside pass 2.  Parts are rounded down to 64 rows.
+  // With pass 1 each lean part is 2/5 of the rows (the middle fifth runs alone), or half
+  // when only the scales are written (lighter, so all of it fits beside the passes); with the
+  // normalisers given (no pass 1) the lean kernel takes the first half (3/5 for scales only)
+  // and nothing runs beside pass 2.  Parts are rounded down to 64 rows.
   const bool pass1 = ga.lse_in == nullptr;
-  const int64_t r_lean = (pass1 ? qa.rows * 2 / 5 : qa.rows / 2) / 64 * 64;
+  const bool codes = qa.vq != nullptr;
+  const int64_t num = pass1 ? (codes ? 2 : 1) : (codes ? 1 : 3), den = pass1 ? (codes ? 5 : 2) : (codes ? 2 : 5);
+  const int64_t r_lean = qa.rows * num / den / 64 * 64;
   const int64_t r_mid_end = pass1 ? qa.rows - r_lean : qa.rows;
   const int64_t vrow = (int64_t)row_bytes_of(qfmt, bits, dims->head_dim);
   auto part = [&](int64_t r0, int64_t r1) {

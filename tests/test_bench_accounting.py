@@ -39,6 +39,13 @@ def test_path_bytes_128k():
     assert per_g["k_quantize"] + per_g["k_quantize_lean"] == LH * n * row
     assert per_g["k_quantize_lean"] == (LH * n // 2 // 64 * 64) * row
     assert bench.LEAN_LAUNCHES == {False: 2, True: 1}
+    # scales only: half beside each pass; with the normalisers given, 3/5 on the second stream
+    per_s, _ = bench.algorithmic_bytes(w, k, full_codes=False)
+    row_s = 2 * w.d + 4
+    assert per_s["k_quantize"] + 2 * per_s["k_quantize_lean"] == LH * n * row_s
+    assert per_s["k_quantize_lean"] == (LH * n // 2 // 64 * 64) * row_s
+    per_gs, _ = bench.algorithmic_bytes(w, k, full_codes=False, normalisers_given=True)
+    assert per_gs["k_quantize_lean"] == (LH * n * 3 // 5 // 64 * 64) * row_s
 
 
 def test_path_bytes_scales_only_and_int4():
