@@ -622,21 +622,27 @@ def test_evict_concurrent_threads(gpu_lib):
 
 def test_evict_without_full_codes(gpu_lib):
     """tp_evict with v_q = NULL (the kept rows are quantised during the compaction): the
-    compact cache, kept set and scores are bit-identical to the run that writes every code."""
+    compact cache, kept set and scores are bit-identical to the run that writes every code,
+    with the normalisers computed and with them supplied (each mode splits step 2 between the
+    two streams differently)."""
     for w in (W.tiny().with_(name="tiny-int4", bits=4),
               W.ragged8().with_(name="ragged-fp8-nocodes", L=2, ctx_lens=(9000, 1, 8193), guide_lens=(32, 128, 7),
                                 keep_budget=500, qfmt=1)):
-        pu.log(f"tp_evict without the full code tensor: {w.describe()}")
         d = B.dims(w.L, w.Hq, w.Hkv, w.d)
         bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
         q, k, v = pu.device_inputs(w)
         kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=w.rule,
                   keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
-        full = B.evict_fused(d, bt, q, k, v, **kw)
-        lean = B.evict_fused(d, bt, q, k, v, full_codes=False, **kw)
-        torch.cuda.synchronize()
-        for n in ("s_key", "scales", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c"):
-            assert torch.equal(getattr(full, n).view(torch.uint8), getattr(lean, n).view(torch.uint8)), (w.name, n)
+        lse = torch.from_numpy(pu.oracle_guide_lse(w).ravel()).cuda()
+        for given in (None, lse):
+            pu.log(f"tp_evict without the full code tensor{' (normalisers given)' if given is not None else ''}: "
+                   f"{w.describe()}")
+            full = B.evict_fused(d, bt, q, k, v, guide_lse=given, **kw)
+            lean = B.evict_fused(d, bt, q, k, v, full_codes=False, guide_lse=given, **kw)
+            torch.cuda.synchronize()
+            for n in ("s_key", "scales", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c"):
+                assert torch.equal(getattr(full, n).view(torch.uint8), getattr(lean, n).view(torch.uint8)), \
+                    (w.name, given is not None, n)
 
 
 def test_evict_profile_events(gpu_lib):
