@@ -180,9 +180,21 @@ def m_lognorm_log2(q_rows, k_rows, scale, kg_rows=None):
     return _orig["guide_log_normalisers"](q_rows, k_rows, scale, kg_rows) / math.log(2.0)
 
 
+def m_bf16_shift_15(bits):
+    bits = np.asarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << 15).view(np.float32).astype(np.float64)
+
+
+def m_bf16_sign_dropped(bits):
+    bits = np.asarray(bits, dtype=np.uint16) & np.uint16(0x7FFF)
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
 # ----------------------------------------------------------------------------- pins to run
 P = pins
 CASES = [
+    ("bf16_to_f64", m_bf16_shift_15, [P.test_bf16_decode_every_pattern]),
+    ("bf16_to_f64", m_bf16_sign_dropped, [P.test_bf16_decode_every_pattern]),
     ("attention_slice", m_softmax_wrong_axis, [P.test_softmax_rows_sum_to_one, P.test_textbook_softmax_reduction]),
     ("attention_slice", m_scale_dropped, [P.test_textbook_softmax_reduction]),
     ("attention_slice", m_transposed_logits, [P.test_textbook_softmax_reduction, P.test_permutation_equivariance]),

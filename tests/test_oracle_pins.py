@@ -22,6 +22,35 @@ def _bf16_round(x):
     return torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
 
 
+# ----------------------------------------------------------------------------- formats
+def _bf16_from_definition(b):
+    """Value of one bf16 bit pattern from the format's definition: 1 sign bit, 8 exponent
+    bits with bias 127, 7 fraction bits; exponent 0 is subnormal (f/128 * 2^-126), 255 is
+    infinity (f = 0) or NaN."""
+    s, e, f = b >> 15, (b >> 7) & 0xFF, b & 0x7F
+    sign = -1.0 if s else 1.0
+    if e == 0xFF:
+        return sign * math.inf if f == 0 else math.nan
+    if e == 0:
+        return sign * math.ldexp(f, -126 - 7)
+    return sign * math.ldexp(128 + f, e - 127 - 7)
+
+
+def test_bf16_decode_every_pattern():
+    """The oracle's bf16 decoder gives, for all 65536 bit patterns (both zeros, subnormals,
+    normals, infinities, NaNs), the value the format defines and the value torch's bfloat16
+    conversion gives."""
+    bits = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = o.bf16_to_f64(bits)
+    ref = np.array([_bf16_from_definition(int(b)) for b in bits.astype(np.int64)])
+    tref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(torch.float64).numpy()
+    for r in (ref, tref):
+        nan = np.isnan(r)
+        assert np.array_equal(np.isnan(got), nan)
+        assert np.array_equal(got[~nan], r[~nan])
+        assert np.array_equal(np.signbit(got[~nan]), np.signbit(r[~nan]))  # -0 stays -0
+
+
 # ----------------------------------------------------------------------------- stage 1
 def test_softmax_rows_sum_to_one():
     """Sec. 6: the attention is softmax-normalised, so each guide row sums to 1 over the
