@@ -276,8 +276,8 @@ class EvictBuffers:
         self.k_c = torch.empty(L * Hkv * max(kt, 1) * D, dtype=torch.bfloat16, device=device)
         self.v_q_c = torch.empty(L * Hkv * max(kt, 1) * rb, dtype=torch.uint8, device=device)
         self.scales_c = torch.empty(L * Hkv * max(kt, 1), dtype=torch.float32, device=device)
-        self.ws_guide = torch.empty(tp_workspace_size(TP_FN_GUIDE_SCORES, d, batch), dtype=torch.uint8,
-                                    device=device)
+        # one workspace serves both paths: tp_evict's holds the score passes' workspace first
+        # (at least TP_FN_GUIDE_SCORES bytes), so evict() hands the same buffer to tp_guide_scores
         self.ws_evict = torch.empty(tp_workspace_size(TP_FN_EVICT, d, batch), dtype=torch.uint8, device=device)
 
 
@@ -288,7 +288,7 @@ def evict(d: TpDims, batch: Batch, q_guide, k, v, *, softmax_scale: float, pool_
     ko = kept_offsets_for(batch, keep_ratio, keep_budget)
     if bufs is None:
         bufs = EvictBuffers(d, batch, qfmt, bits, ko, device=k.device)
-    tp_guide_scores(d, batch, q_guide, k, softmax_scale, pool_k, bufs.s_key, bufs.ws_guide, stream, k_guide)
+    tp_guide_scores(d, batch, q_guide, k, softmax_scale, pool_k, bufs.s_key, bufs.ws_evict, stream, k_guide)
     tp_quantize_v_scales(d, batch, v, qfmt, bits, bufs.scales, bufs.v_q, stream)
     tp_combine_select_topk(d, batch, bufs.s_key, bufs.scales, rule, keep_ratio, keep_budget, ko, bufs.kept_idx,
                            bufs.s_comb, None, stream)

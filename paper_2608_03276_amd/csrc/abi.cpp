@@ -361,6 +361,17 @@ tp_status aux_stream_for(hipStream_t st, AuxStream*& out) {
   return TP_OK;
 }
 
+// After a failed enqueue in tp_evict: record the join event on the second stream (it then
+// completes once everything already queued there has run) and make `st` wait for it.  If the
+// record itself fails, the stream is synchronised instead, so no queued part outlives the
+// call's error return.  Errors here are not reported: the call already fails.
+void join_after_failure(AuxStream* aux, hipStream_t st) {
+  if (hipEventRecord(aux->join, aux->stream) == hipSuccess) {
+    if (hipStreamWaitEvent(st, aux->join, 0) == hipSuccess) return;
+  }
+  (void)hipStreamSynchronize(aux->stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -593,8 +604,15 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr, ev ? ev[5] : nullptr};
   if (e == hipSuccess)
     e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, quant_between, &mid);
+  if (e != hipSuccess) {
+    // Work may already sit on the second stream (it was forked from `st` before the failure):
+    // join it back, best effort, so nothing the caller's stream orders after this call can
+    // overtake a quantisation part still writing the caller's buffers.
+    join_after_failure(aux, st);
+    return hip_fail(e, "tp_evict launch");
+  }
   // the selection reads the scales: wait for the second stream's parts too
-  if (e == hipSuccess) e = hipStreamWaitEvent(st, aux->join, 0);
+  e = hipStreamWaitEvent(st, aux->join, 0);
   if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
   if (e == hipSuccess) e = tp::launch_compact(ca, dims->num_layers * dims->num_kv_heads, dims->head_dim, st);
