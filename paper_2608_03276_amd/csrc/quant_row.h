@@ -20,9 +20,13 @@
 //    other integers: fl32(v * y'') + 1.5 * 2^23; E4M3: the value fl32(v * y'').  A wave
 //    takes this path when every row in it has such a multiplier.
 //  - Corrected quotient otherwise: q0 = v * y, then fl(q0 + fma(-q0, gamma, v) * y), plus
-//    1.5 * 2^23 for an integer code; an exhaustive check over every (A, v) pair of bf16
-//    values, both signs, for every qmax of the supported formats, gives the codes of the
-//    correctly rounded quotient.
+//    1.5 * 2^23 for an integer code.  This is the residual correction of a reciprocal
+//    product used in Markstein's division sequences (P. Markstein, "IA-64 and Elementary
+//    Functions", 2000): the exact remainder v - q0*gamma comes from one fma, and one more
+//    fma adds its scaled value back.  gen_quant_recip.c --replay re-runs this arithmetic
+//    (and every other path below) over every (A, v) pair of bf16 values, both signs, for
+//    every qmax of the supported formats: it gives the codes of the correctly rounded
+//    quotient.
 // No clamp is needed for integer codes since |v/gamma| < qmax + 1/2.  An E4M3 code is the
 // hardware conversion of the value clamped to +-448 (it can exceed 448 by an ulp), with the
 // sign of v.  Every intermediate that can decide a code is a normal number in this range.

@@ -111,28 +111,86 @@ def _exhaustive_block(r0, r1):
     return np.concatenate([a[:, None].astype(np.uint16), v], axis=1)
 
 
+def _no_multiplier_significand(qmax):
+    """A significand t (absmax 1 + t/128) that the one-multiply table marks as having no
+    multiplier for this qmax, or None (read from the committed quant_recip_table.h)."""
+    import os
+    import re
+
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2608_03276_amd", "csrc",
+                        "quant_recip_table.h")
+    text = open(path).read()
+    qs = [float(x) for x in re.search(r"kRecipQmax\[\d+\] = \{([^}]*)\}", text).group(1).replace("f", "").split(",")]
+    masks = re.findall(r"\{\{(0x[0-9a-f]+)ull, (0x[0-9a-f]+)ull\}, \{(0x[0-9a-f]+)ull, (0x[0-9a-f]+)ull\}, "
+                       r"\{(0x[0-9a-f]+)ull, (0x[0-9a-f]+)ull\}\}", text)
+    none = masks[qs.index(float(qmax))][4:6]
+    for t in range(128):
+        if (int(none[t >> 6], 16) >> (t & 63)) & 1:
+            return t
+    return None
+
+
+def _with_poison_rows(rows, poison):
+    """Every 4-row wave of the quantiser (d = 128) gets `poison` as its last row: rows are taken
+    three at a time (the last group padded with zero rows).  Returns the new table and the
+    positions of the original rows in it."""
+    n = rows.shape[0]
+    groups = -(-n // 3)
+    out = np.zeros((groups, 4, rows.shape[1]), dtype=rows.dtype)
+    flat = np.zeros((groups * 3, rows.shape[1]), dtype=rows.dtype)
+    flat[:n] = rows
+    out[:, :3] = flat.reshape(groups, 3, -1)
+    out[:, 3] = poison
+    pos = (np.arange(n) // 3) * 4 + np.arange(n) % 3
+    return out.reshape(groups * 4, -1), pos
+
+
 @pytest.mark.parametrize("qfmt,bits", [(0, 8), (0, 7), (0, 6), (0, 5), (0, 4), (0, 3), (0, 2), (1, 8)])
 def test_quantize_every_pair(gpu_lib, qfmt, bits):
     """Every (absmax, |v| <= absmax) pair of bf16 values, both signs (about 1.07e9 values):
     codes and scales bit-exact against the oracle's definition, for every format (int2 ..
-    int8 and E4M3; each has its own table of one-multiply multipliers)."""
-    pu.log(f"quantize every (absmax, v) pair, qfmt={qfmt} bits={bits}: {_EX_ROWS} rows of 128")
+    int8 and E4M3; each has its own table of one-multiply multipliers).  The path of a row
+    is chosen per wave of 4 rows, so every pair also runs in two more layouts: with an
+    all-zero row in every wave (every row then takes the rescaled path), and with a row whose
+    absmax significand has no one-multiply multiplier in every wave (every row of the common
+    range then takes the corrected quotient; formats without such a significand skip it)."""
+    qmax = 448.0 if qfmt == 1 else float(2 ** (bits - 1) - 1)
+    t_none = _no_multiplier_significand(qmax)
+    poisons = {"zero row": np.zeros(128, dtype=np.uint16)}
+    if t_none is not None:
+        p = np.zeros(128, dtype=np.uint16)
+        p[0] = (127 << 7) | t_none  # absmax (1 + t/128), exponent field 127: the common range
+        poisons["no-multiplier row"] = p
+    pu.log(f"quantize every (absmax, v) pair, qfmt={qfmt} bits={bits}: {_EX_ROWS} rows of 128, "
+           f"layouts: plain, {', '.join(poisons)}")
+    rb = B.row_bytes(qfmt, bits, 128)
+    for name, prow in poisons.items():  # the poison rows' own codes
+        pv = o.bf16_to_f64(prow[None, :])
+        pg = o.value_scales(pv, qfmt, bits)
+        poisons[name] = (prow, pg, o.pack_codes(o.quantize_values(pv, pg, qfmt, bits), qfmt, bits)[0])
     group = 1 << 20
     for g0 in range(0, _EX_ROWS, group):
         rows = _exhaustive_block(g0, min(_EX_ROWS, g0 + group))
         n = rows.shape[0]
-        g, q = _run_quant(rows, 1, 1, [n], 128, qfmt, bits)
-        q = q.reshape(n, B.row_bytes(qfmt, bits, 128))
-        step = 1 << 16
-        for r0 in range(0, n, step):
-            vals = o.bf16_to_f64(rows[r0:r0 + step])
-            gr = o.value_scales(vals, qfmt, bits)
-            qr = o.pack_codes(o.quantize_values(vals, gr, qfmt, bits), qfmt, bits)
-            assert np.array_equal(g[r0:r0 + step].view(np.uint32), gr.view(np.uint32)), f"scales, rows {g0 + r0}+"
-            bad = np.nonzero(np.any(q[r0:r0 + step] != qr, axis=1))[0]
-            assert len(bad) == 0, (f"{len(bad)} rows differ from row {g0 + r0 + bad[0]} "
-                                   f"(absmax bits {hex(int(rows[r0 + bad[0], 0]))})")
-        pu.log(f"  rows {g0} .. {g0 + n} match")
+        vals = o.bf16_to_f64(rows)
+        gr = o.value_scales(vals, qfmt, bits)
+        qr = o.pack_codes(o.quantize_values(vals, gr, qfmt, bits), qfmt, bits)
+        layouts = [("plain", rows, np.arange(n), None)]
+        for name, (prow, pg, pq) in poisons.items():
+            table, pos = _with_poison_rows(rows, prow)
+            layouts.append((name, table, pos, (pg, pq)))
+        for name, table, pos, poison in layouts:
+            g, q = _run_quant(table, 1, 1, [table.shape[0]], 128, qfmt, bits)
+            q = q.reshape(table.shape[0], rb)
+            assert np.array_equal(g[pos].view(np.uint32), gr.view(np.uint32)), f"scales ({name}), rows {g0}+"
+            bad = np.nonzero(np.any(q[pos] != qr, axis=1))[0]
+            assert len(bad) == 0, (f"{name}: {len(bad)} rows differ from row {g0 + bad[0]} "
+                                   f"(absmax bits {hex(int(rows[bad[0], 0]))})")
+            if poison is not None:
+                prow_pos = np.arange(3, table.shape[0], 4)
+                assert np.all(g[prow_pos].view(np.uint32) == poison[0].view(np.uint32)[0]), name
+                assert np.all(q[prow_pos] == poison[1][None, :]), name
+        pu.log(f"  rows {g0} .. {g0 + n} match in every layout")
 
 
 # ----------------------------------------------------------------------------- step 4
