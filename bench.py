@@ -11,6 +11,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -20,6 +21,7 @@ sys.path.insert(0, ROOT)
 METRIC = "context tokens compressed/sec (all layers+heads); achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+FLUSH_BYTES = 512 << 20         # device write between timed steps (larger than every cache)
 
 # The kernels of one tp_evict call, in launch order (the library records an event after each).
 STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_guide_pool", "k_select", "k_compact"]
@@ -130,10 +132,17 @@ def copy_calibration(gib: float = 1.0, reps: int = 3):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
-def _oracle_rate(w, seconds: float, seed: int):
-    """(context tokens/s, segments done, oracle seconds) of the CPU oracle on a random sample
-    of (sequence, layer, KV head) segments; input generation is not timed."""
+def _oracle_rate(w, seconds: float, seed: int, threads: int):
+    """(context tokens/s, segments done, timed wall seconds) of the CPU oracle on a random
+    sample of (sequence, layer, KV head) segments, `threads` segments at a time, each on its
+    own host thread with BLAS limited to one thread (numpy releases the GIL in its array
+    work).  Rounds of `threads` segments: their inputs are generated first (not timed), then
+    the oracle runs on all of them in parallel and the round's wall time is counted, until
+    `seconds` of wall time have been counted."""
+    import concurrent.futures as cf
+
     import numpy as np
+    import threadpoolctl
 
     from oracle import taskpress_oracle as o
 
@@ -141,48 +150,49 @@ def _oracle_rate(w, seconds: float, seed: int):
     import parity_util as pu
 
     segs = [(b, l, h) for b in range(w.batch) for l in range(w.L) for h in range(w.Hkv)]
-    order = np.random.default_rng(seed).permutation(len(segs))
-    done_tokens = 0
-    done = 0
-    elapsed = 0.0
-    for i in order:
-        b, l, h = segs[i]
-        qg, kb, vb = pu.host_segment(w, b, l, h)
-        k = o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget)
-        t0 = time.perf_counter()
+    order = [segs[i] for i in np.random.default_rng(seed).permutation(len(segs))]
+
+    def run(inp):
+        b, qg, kb, vb = inp
         o.evict_segment(qg, kb, vb, softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits,
-                        rule=w.rule, k=k)
-        elapsed += time.perf_counter() - t0
-        done += 1
-        done_tokens += w.ctx_lens[b]
-        if elapsed >= seconds:
-            break
+                        rule=w.rule, k=o.keep_count(w.ctx_lens[b], w.keep_ratio, w.keep_budget))
+        return w.ctx_lens[b]
+
+    done_tokens = done = 0
+    elapsed = 0.0
+    with threadpoolctl.threadpool_limits(limits=1), cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        for r0 in range(0, len(order), threads):
+            if elapsed >= seconds:
+                break
+            inputs = list(ex.map(lambda s: (s[0],) + pu.host_segment(w, *s), order[r0:r0 + threads]))
+            t0 = time.perf_counter()
+            done_tokens += sum(ex.map(run, inputs))
+            elapsed += time.perf_counter() - t0
+            done += len(inputs)
     # a context token counts once all L * Hkv segments of it are done
     return done_tokens / (w.L * w.Hkv) / elapsed, done, elapsed
 
 
 def cpu_baseline(w, seconds: float):
-    """The CPU oracle (test infrastructure) timed on a bounded sample of segments, with the
-    host's BLAS threads and with one thread."""
-    import threadpoolctl
-
+    """The CPU oracle (test infrastructure) timed on a bounded sample of segments, spread over
+    the host's cores (one segment per thread, at most 16 threads: a GPU machine's CPU share), and
+    on one thread."""
+    threads = max(1, min(16, os.cpu_count() or 1))
     segs = w.batch * w.L * w.Hkv
-    rate, done, elapsed = _oracle_rate(w, seconds, 0)
-    with threadpoolctl.threadpool_limits(limits=1):
-        rate1, done1, elapsed1 = _oracle_rate(w, seconds / 3, 1)
-    threads = max([p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()] + [1])
+    rate, done, elapsed = _oracle_rate(w, seconds, 0, threads)
+    rate1, done1, elapsed1 = _oracle_rate(w, seconds / 3, 1, 1)
     cpu = "unknown CPU"
     try:
         with open("/proc/cpuinfo") as f:
             cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
         pass
-    return {"value": rate, "unit": "context tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {segs} (sequence, layer, KV head) segments, {elapsed:.1f} s of oracle time "
-                      f"(numpy float64; BLAS threads = cores; {cpu}, {os.cpu_count()} logical CPUs visible)",
+    return {"value": rate, "unit": "context tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {segs} (sequence, layer, KV head) segments in rounds of {threads}, one segment "
+                      f"per thread, {elapsed:.1f} s of wall time (numpy float64, BLAS at 1 thread per segment; "
+                      f"input generation not timed; {cpu}, {os.cpu_count()} logical CPUs visible)",
             "value_1_thread": rate1,
-            "sample_1_thread": f"{done1} segments (another random order), {elapsed1:.1f} s of oracle time, BLAS "
-                               f"limited to 1 thread"}
+            "sample_1_thread": f"{done1} segments (another random order) on one thread, {elapsed1:.1f} s"}
 
 
 def machine_rates():
@@ -197,6 +207,7 @@ def machine_rates():
     P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
     lib.mb_copy.argtypes = [P, P, I64, I32, P]
     lib.mb_read.argtypes = [P, I64, P, I32, P]
+    lib.mb_two_pass.argtypes = [P, I64, I64, P, I32, P]
     lib.mb_exp.argtypes = [P, I32, I32, P]
     lib.mb_fma.argtypes = [P, I32, I32, P]
     lib.mb_mfma.argtypes = [P, P, I32, I32, P]
@@ -224,6 +235,34 @@ def machine_rates():
             for g in (1024, 4096, 16384)}
     read = {g: nbytes / timed(lambda g=g: lib.mb_read(src.data_ptr(), n16, sink.data_ptr(), g, sp), 5) / 1e9
             for g in (1024, 4096, 16384)}
+    # A buffer read again by the next launch: the second read of X MB against the first (with
+    # 1 GiB of other reads before the first, so it starts cold), median of 5.
+    def once(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        assert fn() == 0
+        b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e-3
+
+    reread = {}
+    for xmb in (32, 64, 128, 192, 256):
+        n = (xmb << 20) // 16
+        first, second = [], []
+        for _ in range(5):
+            assert lib.mb_read(dst.data_ptr(), (1 << 30) // 16, sink.data_ptr(), 4096, sp) == 0
+            first.append(once(lambda: lib.mb_read(src.data_ptr(), n, sink.data_ptr(), 4096, sp)))
+            second.append(once(lambda: lib.mb_read(src.data_ptr(), n, sink.data_ptr(), 4096, sp)))
+        reread[str(xmb)] = {"first_GBps": round((xmb << 20) / sorted(first)[2] / 1e9, 1),
+                            "next_launch_GBps": round((xmb << 20) / sorted(second)[2] / 1e9, 1)}
+    # Two read passes over 4 GiB: whole (the buffer twice) or chunk by chunk (each chunk read
+    # twice in a row by two launches), as a schedule that re-reads K per group of segments would.
+    two_pass = {}
+    for cmb in (0, 32, 64, 128, 256):
+        cb = nbytes if cmb == 0 else cmb << 20
+        grid = 4096 if cmb == 0 else min(4096, cb // 16 // 256 // 4)
+        t = timed(lambda: lib.mb_two_pass(src.data_ptr(), nbytes, cb, sink.data_ptr(), grid, sp), 3)
+        two_pass["whole" if cmb == 0 else f"{cmb}MB_chunks"] = round(2 * nbytes / t / 1e9, 1)
     del src, dst
     blocks, iters = 2048, 4096
     out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
@@ -237,6 +276,8 @@ def machine_rates():
     res = {
         "copy_GBps": {str(g): round(v, 1) for g, v in copy.items()},
         "read_GBps": {str(g): round(v, 1) for g, v in read.items()},
+        "reread_next_launch_by_MB": reread,
+        "two_read_passes_4GiB_GBps": two_pass,
         "exp2_Tps": round(blocks * 256 * iters * 8 / t_exp / 1e12, 2),
         "fma_f32_TFLOPs": round(2 * blocks * 256 * iters * 8 / t_fma / 1e12, 1),
         "mfma_bf16_TFLOPs": round(blocks * 4 * m_iters * 4 * 32768 / t_mfma / 1e12, 1),
@@ -345,20 +386,34 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # Each step is timed by the events the library records at its start and end on this
+    # stream; before each step a 512 MB device write (outside those events) evicts the caches
+    # (4 MB of L2 per XCD, 256 MB Infinity Cache), so no step starts with the previous step's
+    # data cached.  ms_per_step is the median over the K steps.
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.TP_EVICT_EVENTS)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
+        flush.fill_(i & 0xFF)
         step(evs[i])
     end.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
+    step_ms = sorted(e[0].elapsed_time(e[-1]) for e in evs)
+    ms = statistics.median(step_ms)
     stages = STAGES if lse is None else ["pass1_skipped", "k_lse_import"] + STAGES[2:]
     if args.no_full_codes:
         stages = stages[:-1] + ["k_compact_quant"]
-    stage_ms = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(stages)}
+    stage_ms = {n: statistics.median(e[j].elapsed_time(e[j + 1]) for e in evs) for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
+    timing = {"protocol": f"median of {args.steps} steps, each timed by events at its start and end on the "
+                          f"stream it runs on, after {args.warmup} untimed warm-up steps; a {FLUSH_BYTES >> 20} MB "
+                          f"device write before each step (outside its events) evicts the caches; stages_ms are "
+                          f"per-kernel medians",
+              "mean_ms": round(sum(step_ms) / len(step_ms), 4), "min_ms": round(step_ms[0], 4),
+              "max_ms": round(step_ms[-1], 4),
+              "bracket_ms_per_step": round(start.elapsed_time(end) / args.steps, 4)}
 
     per, path_bytes = algorithmic_bytes(w, ko[-1], not args.no_full_codes, lse is not None)
     # the two score passes are bf16 contractions (2 flop per guide-row x token x dim); the
@@ -418,12 +473,13 @@ def main():
         "path_hbm": {"achieved": round(path_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(path_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": path_bytes},
         "path_hbm_measured": measured_path,
+        "timing": timing,
         "stages_ms": {n: round(t, 4) for n, t in stage_ms.items()},
         "kernel_rooflines": {n: {k: v for k, v in roofline_of(n).items()
                                  if k in ("bound", "achieved", "unit", "frac", "other_roof")}
                              for n in stage_ms if n not in ("k_guide_lse", "k_lse_import")},
     }
-    del q, k, v, kg, bufs
+    del q, k, v, kg, bufs, flush
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -1,6 +1,7 @@
 // Microbenchmarks that re-derive, on the machine itself, the ceilings the eviction path is
-// measured against: streaming HBM copy and read bandwidth, the bf16 MFMA rate, the
-// v_exp_f32 and plain fp32 VALU rates, and the shader clock under load.  Measurement only:
+// measured against: streaming HBM copy and read bandwidth, how much a re-read issued by the
+// next launch gains from the caches, the bf16 MFMA rate, the v_exp_f32 and plain fp32 VALU
+// rates, and the shader clock under load.  Measurement only:
 // nothing here is part of the eviction path.  The caller allocates every buffer and times
 // the launches with its own events on `stream`; every kernel stays inside the sizes it is
 // given and every loop has a fixed trip count.
@@ -96,6 +97,21 @@ int mb_copy(const void* src, void* dst, int64_t n16, int grid, void* stream) {
 // sink: device, >= 4 bytes.
 int mb_read(const void* src, int64_t n16, void* sink, int grid, void* stream) {
   hipLaunchKernelGGL(k_read, dim3(grid), dim3(256), 0, (hipStream_t)stream, (const uint4*)src, n16, (uint32_t*)sink);
+  return (int)hipGetLastError();
+}
+
+// Two read passes over `bytes` of src, either whole (chunk_bytes >= bytes: the buffer, then the
+// buffer again) or chunk by chunk (each chunk of chunk_bytes read, then read again at once, the
+// next chunk after that): whether a chunk read again by the next launch comes from a cache.
+// src: device, >= bytes (a multiple of 16); the last chunk is clipped to the buffer.
+int mb_two_pass(const void* src, int64_t bytes, int64_t chunk_bytes, void* sink, int grid, void* stream) {
+  if (chunk_bytes > bytes) chunk_bytes = bytes;
+  for (int64_t off = 0; off < bytes; off += chunk_bytes) {
+    const int64_t len = chunk_bytes < bytes - off ? chunk_bytes : bytes - off;
+    const uint4* p = (const uint4*)((const char*)src + off);
+    for (int r = 0; r < 2; ++r)
+      hipLaunchKernelGGL(k_read, dim3(grid), dim3(256), 0, (hipStream_t)stream, p, len / 16, (uint32_t*)sink);
+  }
   return (int)hipGetLastError();
 }
 
