@@ -197,6 +197,26 @@ tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, con
                                  size_t ws_bytes, void* stream);
 
 /*
+ * Step 3 for callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): tp_combine_select_topk with s_out = NULL
+ * and no workspace argument.  The combined scores are staged in a buffer of
+ * TP_STATIC_SCRATCH_BYTES that the library holds as a static device array, one per GPU its
+ * code is loaded on, kept until the process ends; the call allocates nothing.
+ * Arguments, results and errors as for tp_combine_select_topk, plus TP_ERR_WORKSPACE when
+ * L * Hkv * N_tot * 4 bytes exceed TP_STATIC_SCRATCH_BYTES (validated before anything is
+ * enqueued), and TP_ERR_HIP if the buffer's address on the stream's device cannot be
+ * resolved (done once per device, on the first call there).
+ * Every call on one GPU uses that GPU's one buffer: calls whose work overlaps on a GPU (other
+ * streams, other threads) race and must be ordered by the caller.  The buffer keeps the last
+ * call's contents; each call writes every value it reads.
+ */
+#define TP_STATIC_SCRATCH_BYTES (64u << 20)
+tp_status tp_combine_select_topk_static(const tp_dims* dims, const tp_batch* batch, const float* s_key,
+                                        const float* scales, int32_t rule, double keep_ratio,
+                                        int64_t keep_budget, const int64_t* kept_offsets,
+                                        int32_t* kept_idx, void* stream);
+
+/*
  * Step 4 — compaction (Sec. 3.1: only I is kept; Sec. 4 setup: eviction after
  * prefill, the guide's KV discarded — it is not part of k / v here):
  *   k_out[l][h][ko_b + t][:]      = k[l][h][n0_b + kept_idx[l][h][ko_b + t]][:]

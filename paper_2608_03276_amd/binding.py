@@ -23,7 +23,8 @@ TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
             "tp_guide_scores", "tp_guide_scores_lse", "tp_quantize_v_scales", "tp_combine_select_topk",
-            "tp_compact_kv", "tp_compact_quantize_kv", "tp_evict")
+            "tp_combine_select_topk_static", "tp_compact_kv", "tp_compact_quantize_kv", "tp_evict")
+TP_STATIC_SCRATCH_BYTES = 64 << 20
 
 
 class TaskPressError(RuntimeError):
@@ -116,6 +117,9 @@ def load():
     lib.tp_combine_select_topk.restype = ctypes.c_int32
     lib.tp_combine_select_topk.argtypes = [pd, pb, P, P, ctypes.c_int32, ctypes.c_double, ctypes.c_int64, pi64,
                                            P, P, P, ctypes.c_size_t, P]
+    lib.tp_combine_select_topk_static.restype = ctypes.c_int32
+    lib.tp_combine_select_topk_static.argtypes = [pd, pb, P, P, ctypes.c_int32, ctypes.c_double, ctypes.c_int64,
+                                                  pi64, P, P]
     lib.tp_compact_kv.restype = ctypes.c_int32
     lib.tp_compact_kv.argtypes = [pd, pb, pi64, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, P]
     lib.tp_compact_quantize_kv.restype = ctypes.c_int32
@@ -240,6 +244,20 @@ def tp_combine_select_topk(d: TpDims, batch: Batch, s_key, scales, rule: int, ke
     _check(load().tp_combine_select_topk(ctypes.byref(d), ctypes.byref(batch.c), _ptr(s_key), _ptr(scales),
                                          int(rule), float(keep_ratio), int(keep_budget), ko, _ptr(kept_idx),
                                          _ptr(s_out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def tp_combine_select_topk_static(d: TpDims, batch: Batch, s_key, scales, rule: int, keep_ratio: float,
+                                  keep_budget: int, kept_offsets, kept_idx, stream=None):
+    """Step 3 without a workspace: the combined scores are staged in the library's static
+    device buffer (TP_STATIC_SCRATCH_BYTES per GPU); calls that overlap on one GPU race."""
+    L, Hkv = d.num_layers, d.num_kv_heads
+    _need(s_key, L * Hkv * batch.n_tot * 4, "s_key")
+    _need(scales, L * Hkv * batch.n_tot * 4, "scales")
+    _need(kept_idx, L * Hkv * int(kept_offsets[-1]) * 4, "kept_idx")
+    ko = _i64_array(kept_offsets)
+    _check(load().tp_combine_select_topk_static(ctypes.byref(d), ctypes.byref(batch.c), _ptr(s_key), _ptr(scales),
+                                                int(rule), float(keep_ratio), int(keep_budget), ko, _ptr(kept_idx),
+                                                _stream(stream)))
 
 
 def tp_compact_kv(d: TpDims, batch: Batch, kept_offsets, kept_idx, k, v_q, scales, qfmt: int, bits: int, k_out,

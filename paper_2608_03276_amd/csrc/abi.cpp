@@ -481,6 +481,29 @@ tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, con
   return ok();
 }
 
+tp_status tp_combine_select_topk_static(const tp_dims* dims, const tp_batch* batch, const float* s_key,
+                                        const float* scales, int32_t rule, double keep_ratio, int64_t keep_budget,
+                                        const int64_t* kept_offsets, int32_t* kept_idx, void* stream) {
+  tp::SelectArgs a;
+  // validated as tp_combine_select_topk with the combined scores staged in a buffer of the
+  // static size (a placeholder address here; nothing is enqueued on failure)
+  tp_status s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx,
+                               nullptr, (void*)(uintptr_t)256, tp::kStaticScratchBytes, a);
+  if (s != TP_OK) {
+    if (s == TP_ERR_WORKSPACE)
+      return fail(TP_ERR_WORKSPACE, "the combined scores need %zu bytes, more than the static buffer's %zu",
+                  select_workspace(dims, batch), (size_t)tp::kStaticScratchBytes);
+    return s;
+  }
+  void* buf = nullptr;
+  hipError_t e = tp::static_scratch((hipStream_t)stream, &buf);
+  if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk_static: static buffer");
+  a.s_buf = (float*)buf;
+  e = tp::launch_select(a, dims->num_layers * dims->num_kv_heads, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk_static launch");
+  return ok();
+}
+
 tp_status tp_compact_kv(const tp_dims* dims, const tp_batch* batch, const int64_t* kept_offsets,
                         const int32_t* kept_idx, const void* k, const void* v_q, const float* scales, int32_t qfmt,
                         int32_t bits, void* k_out, void* v_q_out, float* scales_out, void* stream) {

@@ -15,6 +15,8 @@
 //     #(key > T before i) + min(#(key == T before i), need), from one block-wide scan of a
 //     packed (greater, equal) count per tile.
 // Only integer LDS atomics (histogram counts) are used, so the result is deterministic.
+#include <mutex>
+
 #include "tp_internal.h"
 
 namespace tp {
@@ -282,11 +284,47 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   }
 }
 
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];  // per device: its copy of `scratch`, once resolved
+
 }  // namespace
+
+// Staging of the combined scores for tp_combine_select_topk_static (callers that cannot
+// allocate): a file-scope device array, one copy per GPU the library's code is loaded on,
+// kept until the process ends.  In host code `scratch` names a host-side stand-in, never a
+// device address: each GPU's copy is found by hipGetSymbolAddress on that GPU, and only that
+// address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream) {
   hipLaunchKernelGGL(k_select, dim3((unsigned)segments, (unsigned)a.bt.batch), dim3(kSelThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+hipError_t static_scratch(hipStream_t stream, void** ptr) {
+  int dev = 0;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    // once per device, with that device current: the address of its copy of the array
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace tp

@@ -125,6 +125,11 @@ struct SelectArgs {
 };
 hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream);
 
+// The library's static staging buffer for the selection (tp_combine_select_topk_static): the
+// device address of the calling stream's GPU's copy, resolved on the first call on that GPU.
+constexpr size_t kStaticScratchBytes = (size_t)TP_STATIC_SCRATCH_BYTES;
+hipError_t static_scratch(hipStream_t stream, void** ptr);
+
 // ---------------------------------------------------------------- step 4 (compaction)
 struct CompactArgs {
   const int32_t* kept; // [L*Hkv][K_tot]

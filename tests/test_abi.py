@@ -180,6 +180,31 @@ def test_select_validation():
 
 
 @no_gpu
+def test_select_static_validation():
+    """The no-allocation selection validates like tp_combine_select_topk and rejects, before
+    any GPU call, a call whose combined scores exceed the static buffer."""
+    assert B.TP_STATIC_SCRATCH_BYTES == 64 << 20
+
+    def sel(d, bt, ko, rule=0, ratio=0.25, budget=0, kept=FAKE):
+        return lib.tp_combine_select_topk_static(ctypes.byref(d), ctypes.byref(bt.c), FAKE, FAKE, rule, ratio, budget,
+                                                 B._i64_array(ko), kept, None)
+
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300])
+    good = B.kept_offsets_for(bt, 0.25, 0)
+    assert sel(d, bt, good, rule=4) == B.TP_ERR_PARAM
+    assert sel(d, bt, good, ratio=0.25, budget=10) == B.TP_ERR_PARAM
+    assert sel(d, bt, [0, 25, 74]) == B.TP_ERR_SHAPE
+    assert sel(d, bt, good, kept=None) == B.TP_ERR_NULL
+    # one token-head past the limit: L * Hkv * N_tot * 4 = 2^26 + 4 bytes
+    d1 = B.dims(1, 1, 1, 64)
+    n = (64 << 20) // 4 + 1
+    bt1 = B.Batch([0, n])
+    assert sel(d1, bt1, B.kept_offsets_for(bt1, 0.5, 0), ratio=0.5) == B.TP_ERR_WORKSPACE
+    assert "static buffer" in lib.tp_last_error().decode()
+
+
+@no_gpu
 def test_compact_validation():
     d = B.dims(2, 8, 2, 64)
     bt = B.Batch([0, 100, 300])
