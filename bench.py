@@ -23,8 +23,10 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 FLUSH_BYTES = 512 << 20         # device write between timed steps (larger than every cache)
 
-# The kernels of one tp_evict call, in launch order (the library records an event after each).
-STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_guide_pool", "k_select", "k_compact"]
+# The kernels of one tp_evict call, in launch order (the library records an event after each):
+# with the product rule the pooling is part of the selection's first kernel (k_sel_score, which
+# forms the combined scores) and "k_select" is the rest of the selection (four launches).
+STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_sel_score", "k_select", "k_compact"]
 KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
                   "k_guide_lse": ["guide_scores.hip", "tp_internal.h"],
                   "k_guide_attn": ["guide_scores.hip", "tp_internal.h"],
@@ -32,7 +34,8 @@ KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
                   # the rows each step-2 launch takes are set by tp_evict
                   "k_quantize": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
                   "k_quantize_lean": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
-                  "k_select": ["select.hip", "tp_internal.h"],
+                  "k_sel_score": ["select.hip", "tp_internal.h", "abi.cpp"],
+                  "k_select": ["select.hip", "tp_internal.h", "abi.cpp"],
                   "k_compact": ["compact.hip", "tp_internal.h"],
                   "k_compact_quant": ["compact.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h"],
                   "k_lse_import": ["guide_scores.hip", "tp_internal.h"]}
@@ -61,7 +64,8 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True, normalisers_given
         "k_guide_attn": LH * n * (2 * d + 4) + q_bytes,                 # read K, write raw
         "k_guide_pool": LH * n * (4 + 4),                               # read raw, write s_key
         "k_quantize": LH * n * (2 * d + rb + 4),                        # read V, write codes and scales
-        "k_select": LH * (n * (4 + 4 + 4) + kt * 4),                    # read s_key, scales; write S, kept idx
+        "k_sel_score": LH * n * (4 + 4 + 4 + 4),                        # read raw, scales; write s_key, S
+        "k_select": LH * (n * 4 + kt * 4),                              # read S once more, write kept idx
         "k_compact": LH * kt * (2 * (2 * d + rb + 4) + 4),              # read kept rows + idx, write them
         "k_compact_quant": LH * kt * (2 * d + 2 * d + 4 + 2 * d + rb + 4),  # read kept K, V, idx; write
     }
@@ -405,6 +409,8 @@ def main():
     stages = STAGES if lse is None else ["pass1_skipped", "k_lse_import"] + STAGES[2:]
     if args.no_full_codes:
         stages = stages[:-1] + ["k_compact_quant"]
+    if w.rule == B.TP_COMBINE_NORM_ADD:  # its norms need the pooled scores first: a pooling kernel
+        stages[4] = "k_guide_pool"
     stage_ms = {n: statistics.median(e[j].elapsed_time(e[j + 1]) for e in evs) for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
     timing = {"protocol": f"median of {args.steps} steps, each timed by events at its start and end on the "

@@ -22,7 +22,7 @@
  *  - Ownership: the caller allocates every input, output and workspace buffer.
  *    The library allocates no memory and keeps no pointer after returning; buffers
  *    must stay valid until the enqueued work has completed.  (tp_evict keeps one
- *    stream and three events of its own per device: see tp_evict.)
+ *    stream and four events of its own per device: see tp_evict.)
  *  - Execution is asynchronous and stream-ordered; nothing synchronises inside a
  *    call.  Calls are re-entrant.  Results are bit-identical from run to run (no
  *    floating-point atomics; fixed reduction orders).
@@ -186,7 +186,9 @@ tp_status tp_quantize_v_scales(const tp_dims* dims, const tp_batch* batch, const
  * kept_offsets: host [B+1], must equal the prefix sums of k_b (TP_ERR_SHAPE otherwise);
  * kept_idx int32 [L][Hkv][K_tot] (out), K_tot = kept_offsets[B];
  * s_out fp32 [L][Hkv][N_tot] (out, optional): the combined scores S.
- * workspace: >= tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, ...) bytes.
+ * workspace: device, >= tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, ...) bytes, 256-byte
+ * aligned, always required: the combined scores when s_out is NULL, and the per-part counts
+ * of the selection (each segment's tokens are ranked in parts of 8192 by several workgroups).
  * Exactly one of keep_ratio in (0, 1] / keep_budget >= 1 must be given (the other
  * <= 0), otherwise TP_ERR_PARAM.
  */
@@ -199,13 +201,14 @@ tp_status tp_combine_select_topk(const tp_dims* dims, const tp_batch* batch, con
 /*
  * Step 3 for callers that cannot allocate device memory (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): tp_combine_select_topk with s_out = NULL
- * and no workspace argument.  The combined scores are staged in a buffer of
- * TP_STATIC_SCRATCH_BYTES that the library holds as a static device array, one per GPU its
- * code is loaded on, kept until the process ends; the call allocates nothing.
+ * and no workspace argument.  The combined scores and the selection's counts are staged in a
+ * buffer of TP_STATIC_SCRATCH_BYTES that the library holds as a static device array, one per
+ * GPU its code is loaded on, kept until the process ends; the call allocates nothing.
  * Arguments, results and errors as for tp_combine_select_topk, plus TP_ERR_WORKSPACE when
- * L * Hkv * N_tot * 4 bytes exceed TP_STATIC_SCRATCH_BYTES (validated before anything is
- * enqueued), and TP_ERR_HIP if the buffer's address on the stream's device cannot be
- * resolved (done once per device, on the first call there).
+ * the selection's workspace (tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, ...), about
+ * 5 bytes per token and segment plus 32 KB per segment and sequence) exceeds TP_STATIC_SCRATCH_BYTES (validated before
+ * anything is enqueued), and TP_ERR_HIP if the buffer's address on the stream's device
+ * cannot be resolved (done once per device, on the first call there).
  * Every call on one GPU uses that GPU's one buffer: calls whose work overlaps on a GPU (other
  * streams, other threads) race and must be ordered by the caller.  The buffer keeps the last
  * call's contents; each call writes every value it reads.
@@ -279,7 +282,7 @@ typedef struct tp_profile {
  * Step 2 of most V rows runs on a second stream of the library's: 2/5 concurrently with each
  * score pass (half with each when v_q is NULL), or, with guide_lse given, the first half
  * (3/5 when v_q is NULL) concurrently with the rest of the step; the arithmetic is the same,
- * so the results are as for the separate calls.  That stream and three events are created, with default priority, by the first
+ * so the results are as for the separate calls.  That stream and four events are created, with default priority, by the first
  * tp_evict call on a device and kept until the process ends (TP_ERR_HIP if that fails); the
  * work is forked from and joined back to `stream`, so the call stays stream-ordered and may
  * be captured into a graph (once the first call on the device, which creates the stream,

@@ -240,7 +240,10 @@ def tp_combine_select_topk(d: TpDims, batch: Batch, s_key, scales, rule: int, ke
     _need(kept_idx, L * Hkv * int(kept_offsets[-1]) * 4, "kept_idx")
     _need(s_out, L * Hkv * batch.n_tot * 4, "s_out")
     ko = _i64_array(kept_offsets)
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    if workspace is None:  # the caller passed none: one of the size the library asks for
+        workspace = torch.empty(tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, d, batch), dtype=torch.uint8,
+                                device=s_key.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
     _check(load().tp_combine_select_topk(ctypes.byref(d), ctypes.byref(batch.c), _ptr(s_key), _ptr(scales),
                                          int(rule), float(keep_ratio), int(keep_budget), ko, _ptr(kept_idx),
                                          _ptr(s_out), _ptr(workspace), ws_bytes, _stream(stream)))

@@ -88,8 +88,7 @@ tp_status hip_fail(hipError_t e, const char* where) {
 }
 
 size_t select_workspace(const tp_dims* d, const tp_batch* bt) {
-  const size_t n = (size_t)d->num_layers * d->num_kv_heads * (size_t)bt->ctx_offsets[bt->batch];
-  return ((n * sizeof(float)) + 255) & ~(size_t)255;
+  return tp::select_workspace_layout((int64_t)d->num_layers * d->num_kv_heads, bt->ctx_offsets, bt->batch).total;
 }
 
 // Largest quantised magnitude (Eq. 2): 2^(b-1) - 1 for b-bit integers, 448 for E4M3.
@@ -228,17 +227,39 @@ tp_status prepare_select(const tp_dims* dims, const tp_batch* batch, const float
     a.kept_off[b] = kept_offsets[b];
   }
   a.kept_off[batch->batch] = kept_offsets[batch->batch];
-  float* sbuf = s_out;
-  if (!sbuf) {
-    const size_t need = select_workspace(dims, batch);
-    if (!workspace || ws_bytes < need)
-      return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu)", need, ws_bytes);
-    if (!aligned16(workspace)) return fail(TP_ERR_WORKSPACE, "workspace must be 16-byte aligned");
-    sbuf = (float*)workspace;
-  }
+  const int64_t segs = (int64_t)dims->num_layers * dims->num_kv_heads;
+  const tp::SelectWorkspace lay = tp::select_workspace_layout(segs, batch->ctx_offsets, batch->batch);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu%s)", lay.total, ws_bytes,
+                workspace ? "" : ", NULL");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(TP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  char* ws = (char*)workspace;
   a.s_key = s_key;
   a.scales = scales;
-  a.s_buf = sbuf;
+  a.s_buf = s_out ? s_out : (float*)(ws + lay.s_off);
+  a.hist = (uint32_t*)(ws + lay.hist_off);
+  a.info = (uint4*)(ws + lay.info_off);
+  a.thr = (uint2*)(ws + lay.thr_off);
+  a.pcount = (uint2*)(ws + lay.pcount_off);
+  a.pref = (uint2*)(ws + lay.pref_off);
+  a.cstart = (uint32_t*)(ws + lay.cstart_off);
+  a.cand = (uint32_t*)(ws + lay.cand_off);
+  a.part_tot = lay.part_tot;
+  a.cand_tot = lay.cand_tot;
+  a.part_off[0] = a.cand_off[0] = 0;
+  int64_t part_max = 0;
+  for (int b = 0; b < batch->batch; ++b) {
+    const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    const int64_t np = (nb + tp::kSelPartTokens - 1) / tp::kSelPartTokens;
+    part_max = std::max(part_max, np);
+    a.part_off[b + 1] = a.part_off[b] + np;
+    a.cand_off[b + 1] = a.cand_off[b] + std::min<int64_t>(nb, tp::kSelCandCap);
+  }
+  if (part_max > 65535) return fail(TP_ERR_UNSUPPORTED, "a sequence of more than %lld context tokens",
+                                    (long long)65535 * tp::kSelPartTokens);
+  a.part_max = (int32_t)part_max;
+  a.raw = nullptr;  // the key score is read (tp_evict sets the fused pooling)
+  a.s_key_out = nullptr;
   a.kept = kept_idx;
   a.n_tot = batch->ctx_offsets[batch->batch];
   a.k_tot = kept_offsets[batch->batch];
@@ -321,14 +342,14 @@ size_t evict_workspace_bytes(const tp_dims* dims, const tp_batch* batch) {
 }
 
 // The second stream of tp_evict on one device and the events that fork it from, and join it
-// to, the caller's stream: created by the first tp_evict call on that device and kept until
+// to, the caller's stream (part1: the first part of step 2 on it is done): created by the first tp_evict call on that device and kept until
 // the process ends.  `enqueue` is held while a call enqueues its work, so calls from several
 // threads do not interleave their uses of the events.
 struct AuxStream {
   std::mutex enqueue;
   bool ready = false;
   hipStream_t stream = nullptr;
-  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr, part1 = nullptr;
 };
 constexpr int kMaxDevices = 64;
 AuxStream g_aux[kMaxDevices];
@@ -350,6 +371,7 @@ tp_status aux_stream_for(hipStream_t st, AuxStream*& out) {
     if (e == hipSuccess && !a.fork) e = hipEventCreateWithFlags(&a.fork, hipEventDisableTiming);
     if (e == hipSuccess && !a.fork2) e = hipEventCreateWithFlags(&a.fork2, hipEventDisableTiming);
     if (e == hipSuccess && !a.join) e = hipEventCreateWithFlags(&a.join, hipEventDisableTiming);
+    if (e == hipSuccess && !a.part1) e = hipEventCreateWithFlags(&a.part1, hipEventDisableTiming);
     if (cur != dev) {
       const hipError_t e2 = hipSetDevice(cur);
       if (e == hipSuccess) e = e2;
@@ -359,6 +381,20 @@ tp_status aux_stream_for(hipStream_t st, AuxStream*& out) {
   }
   out = &a;
   return TP_OK;
+}
+
+// The selection's workspace pointers, laid out from `from`, moved to the same offsets from `to`.
+char* const kPlaceholder = (char*)(uintptr_t)256;  // a 256-byte-aligned stand-in, never dereferenced
+void rebase_select(tp::SelectArgs& a, char* from, char* to) {
+  auto mv = [&](auto* p) { return (decltype(p))(to + ((char*)p - from)); };
+  a.s_buf = mv(a.s_buf);
+  a.hist = mv(a.hist);
+  a.info = mv(a.info);
+  a.thr = mv(a.thr);
+  a.pcount = mv(a.pcount);
+  a.pref = mv(a.pref);
+  a.cstart = mv(a.cstart);
+  a.cand = mv(a.cand);
 }
 
 // After a failed enqueue in tp_evict: record the join event on the second stream (it then
@@ -488,17 +524,17 @@ tp_status tp_combine_select_topk_static(const tp_dims* dims, const tp_batch* bat
   // validated as tp_combine_select_topk with the combined scores staged in a buffer of the
   // static size (a placeholder address here; nothing is enqueued on failure)
   tp_status s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx,
-                               nullptr, (void*)(uintptr_t)256, tp::kStaticScratchBytes, a);
+                               nullptr, kPlaceholder, tp::kStaticScratchBytes, a);
   if (s != TP_OK) {
     if (s == TP_ERR_WORKSPACE)
-      return fail(TP_ERR_WORKSPACE, "the combined scores need %zu bytes, more than the static buffer's %zu",
+      return fail(TP_ERR_WORKSPACE, "the selection needs %zu bytes of workspace, more than the static buffer's %zu",
                   select_workspace(dims, batch), (size_t)tp::kStaticScratchBytes);
     return s;
   }
   void* buf = nullptr;
   hipError_t e = tp::static_scratch((hipStream_t)stream, &buf);
   if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk_static: static buffer");
-  a.s_buf = (float*)buf;
+  rebase_select(a, kPlaceholder, (char*)buf);
   e = tp::launch_select(a, dims->num_layers * dims->num_kv_heads, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tp_combine_select_topk_static launch");
   return ok();
@@ -557,6 +593,19 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx, s_out,
                      (char*)workspace + gws, ews - gws, sa);
   if (s != TP_OK) return s;
+  // Every rule but NORM_ADD (whose norms need the pooled scores first) pools score pass 2's
+  // raw sums inside the selection's first kernel, which writes s_key: no pooling kernel.
+  const bool fuse_pool = rule != TP_COMBINE_NORM_ADD;
+  if (fuse_pool) {
+    ga.skip_pool = 1;
+    sa.raw = ga.raw;
+    sa.s_key_out = s_key;
+    sa.pool_inv = ga.pool_inv;
+    sa.pool_half = ga.pool_half;
+    for (int b = 0; b < batch->batch; ++b)
+      sa.nrg[b] = (int32_t)((ga.R * (batch->guide_offsets[b + 1] - batch->guide_offsets[b]) + tp::kRowsPerGroup - 1) /
+                            tp::kRowsPerGroup);
+  }
   tp::CompactArgs ca;
   // without v_q the codes of the evicted rows are never written: the compaction quantises
   // the kept V rows itself (same codes and scales)
@@ -603,6 +652,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   if (e == hipSuccess) e = hipEventRecord(aux->fork, st);
   if (e == hipSuccess) e = hipStreamWaitEvent(aux->stream, aux->fork, 0);
   if (e == hipSuccess) e = tp::launch_quantize_lean(qa1, dims->head_dim, aux->stream);
+  if (e == hipSuccess) e = hipEventRecord(aux->part1, aux->stream);  // the first part's scales are written
   // called by the score pass between the normalisers and pass 2 (exactly once on success)
   struct Mid {
     const tp::QuantArgs* mid;
@@ -624,9 +674,28 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
     if (r == hipSuccess) r = hipEventRecord(m->aux->join, m->aux->stream);
     return r;
   };
-  hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr, ev ? ev[5] : nullptr};
+  hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr,
+                       ev && !fuse_pool ? ev[5] : nullptr};
   if (e == hipSuccess)
     e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, quant_between, &mid);
+  // The selection reads the scales.  Segments whose V rows all belong to parts of step 2
+  // already done in this stream's order form their combined scores while the second stream
+  // finishes its last part; the rest wait for it.  With pass 1 those are the rows before the
+  // part beside pass 2 (the first part, on the second stream, is waited for by its own
+  // event); with the normalisers given, the rows after the second stream's part.
+  const int segs = dims->num_layers * dims->num_kv_heads;
+  const int64_t n_tot = batch->ctx_offsets[batch->batch];
+  int rb = 0, re = 0;  // segments [rb, re) scored before the join
+  if (fuse_pool) {
+    if (pass1) {
+      re = (int)std::min<int64_t>(segs, r_mid_end / n_tot);
+    } else {
+      rb = (int)std::min<int64_t>(segs, (r_lean + n_tot - 1) / n_tot);
+      re = segs;
+    }
+  }
+  if (e == hipSuccess && re > rb && pass1) e = hipStreamWaitEvent(st, aux->part1, 0);
+  if (e == hipSuccess) e = tp::launch_select_score(sa, rb, re, segs, st);
   if (e != hipSuccess) {
     // Work may already sit on the second stream (it was forked from `st` before the failure):
     // join it back, best effort, so nothing the caller's stream orders after this call can
@@ -634,9 +703,8 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
     join_after_failure(aux, st);
     return hip_fail(e, "tp_evict launch");
   }
-  // the selection reads the scales: wait for the second stream's parts too
   e = hipStreamWaitEvent(st, aux->join, 0);
-  if (e == hipSuccess) e = tp::launch_select(sa, dims->num_layers * dims->num_kv_heads, st);
+  if (e == hipSuccess) e = tp::launch_select(sa, segs, st, ev && fuse_pool ? ev[5] : nullptr, rb, re);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
   if (e == hipSuccess) e = tp::launch_compact(ca, dims->num_layers * dims->num_kv_heads, dims->head_dim, st);
   if (e == hipSuccess && ev) e = hipEventRecord(ev[7], st);

@@ -765,10 +765,11 @@ hipError_t launch_d(const GuideArgs& a, hipStream_t stream, hipEvent_t* ev, Guid
       if (e != hipSuccess) return e;
     }
   }
+  if (a.skip_pool) return hipSuccess;  // the split selection pools the raw sums itself
   const dim3 pgrid((unsigned)((max_nb + kPoolTile - 1) / kPoolTile), (unsigned)(a.L * a.Hkv), (unsigned)a.bt.batch);
   hipLaunchKernelGGL(k_guide_pool, pgrid, dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[3], stream);
+  if (e == hipSuccess && ev && ev[3]) e = hipEventRecord(ev[3], stream);
   return e;
 }
 

@@ -56,6 +56,8 @@ struct GuideArgs {
   // first workgroup of each sequence's range in the score passes: sequence b has
   // ceil(L * Hkv * nchunk_b / 8) * 8 * nrg_b workgroups
   int32_t wg_off[TP_MAX_BATCH + 1];
+  // the pooling kernel is left out (the split selection pools the raw sums itself)
+  int32_t skip_pool;
 };
 
 struct GuideWorkspace {
@@ -111,8 +113,13 @@ hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream)
 hipError_t launch_quantize_lean(const QuantArgs& a, int head_dim, hipStream_t stream);
 
 // ---------------------------------------------------------------- step 3 (select)
+// Every rule but NORM_ADD runs the split selection: each segment's tokens are cut into parts
+// of kSelPartTokens, one workgroup per part in the passes over the scores.
+constexpr int kSelPartTokens = 8192;
+constexpr int kSelCandCap = 8192;  // keys of the threshold's top-digit bucket kept per segment
+
 struct SelectArgs {
-  const float* s_key;  // fp32 [L*Hkv][N_tot]
+  const float* s_key;  // fp32 [L*Hkv][N_tot]  (read unless `raw` is set)
   const float* scales; // fp32 [L*Hkv][N_tot]
   float* s_buf;        // fp32 [L*Hkv][N_tot]   combined scores (s_out or workspace)
   int32_t* kept;       // int32 [L*Hkv][K_tot]
@@ -122,8 +129,44 @@ struct SelectArgs {
   int64_t k[TP_MAX_BATCH];
   int64_t kept_off[TP_MAX_BATCH + 1];
   BatchArgs bt;
+  // Pooling fused into the split selection (tp_evict): the key score is pooled here from score
+  // pass 2's per-row-group sums and written to s_key_out; nullptr reads s_key instead.
+  const float* raw;    // [nrg][L*Hkv][N_tot]
+  float* s_key_out;    // fp32 [L*Hkv][N_tot]
+  float pool_inv;      // 1 / (R * pool_k)
+  int32_t pool_half;   // pool_k / 2
+  int32_t nrg[TP_MAX_BATCH];  // row groups of sequence b
+  // Workspace of the split selection (select_workspace_layout):
+  uint32_t* hist;      // [L*Hkv][part_tot][kBins/2]  per-part top-digit counts, two 16-bit per word
+  uint4* info;         // [L*Hkv][batch]  top digit of the k-th key, keys still needed, bucket size
+  uint2* thr;          // [L*Hkv][batch]  threshold key T, keys equal to T to keep
+  uint2* pcount;       // [L*Hkv][part_tot]  per part: keys above the top digit, keys in it
+  uint2* pref;         // [L*Hkv][part_tot]  per part: keys > T and keys == T in earlier parts
+  uint32_t* cstart;    // [L*Hkv][part_tot]  per part: its first slot in the candidate list
+  uint32_t* cand;      // [L*Hkv][cand_tot]  the top-digit bucket's keys
+  int64_t part_tot, cand_tot;
+  int64_t part_off[TP_MAX_BATCH + 1];  // parts of the sequences before b
+  int64_t cand_off[TP_MAX_BATCH + 1];  // candidate slots of the sequences before b
+  int32_t part_max;    // parts of the longest sequence
+  int32_t pad2_;
 };
-hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream);
+
+struct SelectWorkspace {
+  size_t s_off, hist_off, info_off, thr_off, pcount_off, pref_off, cstart_off, cand_off, total;
+  int64_t part_tot, cand_tot;
+};
+// Layout of the selection's workspace: the combined scores (unless s_out is given), then the
+// split selection's buffers.  segments = L * Hkv.
+SelectWorkspace select_workspace_layout(int64_t segments, const int64_t* ctx_off, int32_t batch);
+
+// after_score (optional): recorded once the combined scores are formed (after the pooling
+// fused into the split selection, when `raw` is set).  [scored_begin, scored_end): segments
+// whose combined scores launch_select_score has already enqueued (the split selection only).
+hipError_t launch_select(const SelectArgs& a, int segments, hipStream_t stream, hipEvent_t after_score = nullptr,
+                         int scored_begin = 0, int scored_end = 0);
+// The split selection's first kernel for segments [seg_begin, seg_end) of `segments` (none for
+// NORM_ADD), so a caller can form the scores of segments whose inputs are ready early.
+hipError_t launch_select_score(const SelectArgs& a, int seg_begin, int seg_end, int segments, hipStream_t stream);
 
 // The library's static staging buffer for the selection (tp_combine_select_topk_static): the
 // device address of the calling stream's GPU's copy, resolved on the first call on that GPU.

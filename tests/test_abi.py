@@ -177,6 +177,10 @@ def test_select_validation():
     assert sel(ko=[1, 26, 76]) == B.TP_ERR_SHAPE
     assert sel(kept=None) == B.TP_ERR_NULL
     assert sel(s_out=None) == B.TP_ERR_WORKSPACE  # no s_out and no workspace
+    assert sel() == B.TP_ERR_WORKSPACE  # the workspace is required with s_out too
+    ws = B.tp_workspace_size(B.TP_FN_COMBINE_SELECT_TOPK, d, bt)
+    assert sel(ws=FAKE, wsb=ws - 1) == B.TP_ERR_WORKSPACE
+    assert sel(ws=FAKE + 16, wsb=ws) == B.TP_ERR_WORKSPACE  # not 256-byte aligned
 
 
 @no_gpu
@@ -196,7 +200,7 @@ def test_select_static_validation():
     assert sel(d, bt, good, ratio=0.25, budget=10) == B.TP_ERR_PARAM
     assert sel(d, bt, [0, 25, 74]) == B.TP_ERR_SHAPE
     assert sel(d, bt, good, kept=None) == B.TP_ERR_NULL
-    # one token-head past the limit: L * Hkv * N_tot * 4 = 2^26 + 4 bytes
+    # past the limit: the combined scores alone take 2^26 + 4 bytes
     d1 = B.dims(1, 1, 1, 64)
     n = (64 << 20) // 4 + 1
     bt1 = B.Batch([0, n])

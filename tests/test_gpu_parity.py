@@ -478,11 +478,14 @@ def test_guide_scores_lse_parity(gpu_lib, case, jitter):
 
 # ----------------------------------------------------------------------------- whole path
 @pytest.mark.parametrize("rule", [0, 3])
-def test_end_to_end_tiny(gpu_lib, rule):
+@pytest.mark.parametrize("fused", [False, True])
+def test_end_to_end_tiny(gpu_lib, rule, fused):
+    """Every rule against the oracle, through the four calls and through tp_evict (which pools
+    inside the selection for every rule but NORM_ADD)."""
     w = W.tiny()
-    pu.log(f"end-to-end {w.describe()} rule={rule}")
+    pu.log(f"end-to-end {w.describe()} rule={rule} fused={fused}")
     q, k, v = pu.device_inputs(w)
-    bufs = pu.run_gpu(w, q, k, v, rule=rule)
+    bufs = pu.run_gpu(w, q, k, v, rule=rule, fused=fused)
     for l in range(w.L):
         for h in range(w.Hkv):
             pu.check_segment(w, bufs, 0, l, h, rule=rule)
@@ -539,7 +542,13 @@ def test_evict_matches_the_four_calls(gpu_lib):
               # fewer than 192 V rows (the second stream's parts are empty), and a middle part
               # that is not a whole number of 64-row groups
               W.tiny().with_(name="tiny-61-rows", Hq=2, Hkv=1, ctx_lens=(1, 60), guide_lens=(3, 2)),
-              W.tiny().with_(name="tiny-401-rows", Hq=4, Hkv=1, ctx_lens=(333, 68), guide_lens=(5, 7))):
+              W.tiny().with_(name="tiny-401-rows", Hq=4, Hkv=1, ctx_lens=(333, 68), guide_lens=(5, 7)),
+              # the pooling fused into the selection: staged windows of the widest staged
+              # half-width (512) and wider ones summed directly, a window wider than the
+              # sequence, and sequences of several 32768-token parts of the selection
+              W.tiny().with_(name="wide-pool-staged", ctx_lens=(2500, 40, 3), guide_lens=(4, 2, 9), pool_k=1025),
+              W.tiny().with_(name="wide-pool-direct", ctx_lens=(3000, 2), guide_lens=(4, 6), pool_k=1027),
+              W.tiny().with_(name="three-parts", ctx_lens=(70001, 5, 32768), guide_lens=(8, 3, 20), keep_ratio=0.3)):
         pu.log(f"tp_evict vs four calls: {w.describe()}")
         _fused_vs_calls(w)
 
