@@ -180,6 +180,26 @@ def guide_log_normalisers(q_rows: np.ndarray, k_rows: np.ndarray, softmax_scale:
     return m + np.log(np.exp(x - m[:, None]).sum(axis=1))
 
 
+def guide_attention_output(q_rows: np.ndarray, k_rows: np.ndarray, v_rows: np.ndarray, softmax_scale: float,
+                           kg_rows: np.ndarray | None = None, vg_rows: np.ndarray | None = None) -> np.ndarray:
+    """Output of the prefill's attention for the guide rows (Sec. 3.2: the guide is appended
+    after the context and attends causally): row j is the softmax-weighted sum of the values
+    of the keys it sees, the N context keys, plus guide keys 0..j when kg_rows / vg_rows [G, d]
+    are given.  q_rows [G, d], k_rows / v_rows [N, d] -> [G, d], float64.  Its normaliser is
+    guide_log_normalisers' (the weights of the context keys are attention_slice's)."""
+    x = softmax_scale * (q_rows @ k_rows.T)
+    if kg_rows is None:
+        m = x.max(axis=1, keepdims=True)
+        e = np.exp(x - m)
+        return (e @ v_rows) / e.sum(axis=1, keepdims=True)
+    g = q_rows.shape[0]
+    y = softmax_scale * (q_rows @ kg_rows.T)
+    y = np.where(np.arange(g)[None, :] <= np.arange(g)[:, None], y, -np.inf)  # guide key t seen by row j iff t <= j
+    m = np.maximum(x.max(axis=1, keepdims=True), y.max(axis=1, keepdims=True))
+    e, eg = np.exp(x - m), np.exp(y - m)
+    return (e @ v_rows + eg @ vg_rows) / (e.sum(axis=1, keepdims=True) + eg.sum(axis=1, keepdims=True))
+
+
 def guide_attention_sum_given_lse(q_group: np.ndarray, k_rows: np.ndarray, softmax_scale: float,
                                   lse: np.ndarray) -> np.ndarray:
     """Inner sum of Eq. 1 with the normaliser supplied by the caller (Sec. 3.2 slices A from

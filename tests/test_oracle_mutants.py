@@ -190,6 +190,36 @@ def m_bf16_sign_dropped(bits):
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def m_output_not_causal_self(q_rows, k_rows, v_rows, scale, kg_rows=None, vg_rows=None):
+    if kg_rows is None:
+        return _orig["guide_attention_output"](q_rows, k_rows, v_rows, scale)
+    g = q_rows.shape[0]
+    x = scale * (q_rows @ k_rows.T)
+    y = scale * (q_rows @ kg_rows.T)
+    y = np.where(np.arange(g)[None, :] < np.arange(g)[:, None], y, -np.inf)  # own key left out
+    m = np.maximum(x.max(axis=1, keepdims=True), np.max(np.where(np.isinf(y), -1e300, y), axis=1, keepdims=True))
+    e, eg = np.exp(x - m), np.exp(y - m)
+    return (e @ v_rows + eg @ vg_rows) / (e.sum(axis=1, keepdims=True) + eg.sum(axis=1, keepdims=True))
+
+
+def m_output_context_normaliser(q_rows, k_rows, v_rows, scale, kg_rows=None, vg_rows=None):
+    if kg_rows is None:
+        return _orig["guide_attention_output"](q_rows, k_rows, v_rows, scale)
+    g = q_rows.shape[0]
+    x = scale * (q_rows @ k_rows.T)
+    y = scale * (q_rows @ kg_rows.T)
+    y = np.where(np.arange(g)[None, :] <= np.arange(g)[:, None], y, -np.inf)
+    m = np.maximum(x.max(axis=1, keepdims=True), y.max(axis=1, keepdims=True))
+    e, eg = np.exp(x - m), np.exp(y - m)
+    return (e @ v_rows + eg @ vg_rows) / e.sum(axis=1, keepdims=True)  # guide keys left out of the normaliser
+
+
+def m_output_guide_values_shifted(q_rows, k_rows, v_rows, scale, kg_rows=None, vg_rows=None):
+    if kg_rows is None:
+        return _orig["guide_attention_output"](q_rows, k_rows, v_rows, scale)
+    return _orig["guide_attention_output"](q_rows, k_rows, v_rows, scale, kg_rows, np.roll(vg_rows, 1, axis=0))
+
+
 # ----------------------------------------------------------------------------- pins to run
 P = pins
 CASES = [
@@ -220,6 +250,12 @@ CASES = [
     ("guide_log_normalisers", m_lognorm_not_causal_self, [P.test_log_normalisers_closed_form]),
     ("guide_log_normalisers", m_lognorm_log2, [P.test_log_normalisers_closed_form,
                                                 P.test_log_normalisers_vs_scipy_logsumexp]),
+    ("guide_attention_output", m_output_not_causal_self,
+     [P.test_guide_attention_output_matches_the_full_causal_attention, P.test_guide_attention_output_closed_forms]),
+    ("guide_attention_output", m_output_context_normaliser,
+     [P.test_guide_attention_output_matches_the_full_causal_attention, P.test_guide_attention_output_closed_forms]),
+    ("guide_attention_output", m_output_guide_values_shifted,
+     [P.test_guide_attention_output_matches_the_full_causal_attention, P.test_guide_attention_output_closed_forms]),
 ]
 
 

@@ -177,6 +177,54 @@ def _full_causal_map(q_ctx, k_ctx, q_guide, k_guide, scale):
     return out[n:, :n]
 
 
+def _full_causal_outputs(q_ctx, k_ctx, v_ctx, q_guide, k_guide, v_guide, scale):
+    """Brute force: the guide rows' outputs of the full causal attention over the context
+    with the guide appended (softmax of each row over keys 0..p, times the values)."""
+    qa = np.concatenate([q_ctx, q_guide])
+    ka = np.concatenate([k_ctx, k_guide])
+    va = np.concatenate([v_ctx, v_guide])
+    n = q_ctx.shape[0]
+    out = []
+    for p in range(n, qa.shape[0]):
+        logits = [scale * float(np.dot(qa[p], ka[t])) for t in range(p + 1)]
+        m = max(logits)
+        w = [math.exp(v - m) for v in logits]
+        z = math.fsum(w)
+        out.append([math.fsum(w[t] * va[t, c] for t in range(p + 1)) / z for c in range(va.shape[1])])
+    return np.array(out)
+
+
+def test_guide_attention_output_matches_the_full_causal_attention():
+    """The prefill's attention output for the appended guide rows (Sec. 3.2): equal to the
+    guide rows of the full causal attention over context + guide, built by brute force."""
+    for N, G, d, scale in [(5, 3, 4, 0.7), (12, 6, 8, 0.35), (1, 4, 2, 1.1)]:
+        q_ctx = rng.standard_normal((N, d))
+        k_ctx, v_ctx = rng.standard_normal((N, d)) * 2, rng.standard_normal((N, d))
+        q_g, k_g, v_g = rng.standard_normal((G, d)) * 2, rng.standard_normal((G, d)) * 2, rng.standard_normal((G, d))
+        want = _full_causal_outputs(q_ctx, k_ctx, v_ctx, q_g, k_g, v_g, scale)
+        got = o.guide_attention_output(q_g, k_ctx, v_ctx, scale, k_g, v_g)
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-13)
+
+
+def test_guide_attention_output_closed_forms():
+    """One row without guide keys is softmax(s K q) V (scipy); constant values come out
+    unchanged (the weights sum to 1); Q = 0 averages the values each row sees."""
+    N, G, d = 40, 5, 8
+    k, v = rng.standard_normal((N, d)), rng.standard_normal((N, d))
+    q = rng.standard_normal((1, d))
+    np.testing.assert_allclose(o.guide_attention_output(q, k, v, 0.4)[0],
+                               scipy.special.softmax(0.4 * (k @ q[0])) @ v, rtol=1e-12)
+    c = rng.standard_normal(d)
+    kg = rng.standard_normal((G, d))
+    q5 = rng.standard_normal((G, d)) * 3
+    out = o.guide_attention_output(q5, k, np.tile(c, (N, 1)), 0.5, kg, np.tile(c, (G, 1)))
+    np.testing.assert_allclose(out, np.tile(c, (G, 1)), rtol=1e-12, atol=1e-12)
+    vg = rng.standard_normal((G, d))
+    out0 = o.guide_attention_output(np.zeros((G, d)), k, v, 0.5, kg, vg)
+    for j in range(G):
+        np.testing.assert_allclose(out0[j], (v.sum(axis=0) + vg[:j + 1].sum(axis=0)) / (N + j + 1), rtol=1e-12)
+
+
 def test_guide_keys_match_the_full_causal_map():
     """With the guide's keys, A is the context slice of the causal attention map of the
     context with the guide appended (Sec. 3.2), checked by building that map."""
