@@ -27,10 +27,11 @@ FLUSH_BYTES = 512 << 20         # device write between timed steps (larger than 
 # with the product rule the pooling is part of the selection's first kernel (k_sel_score, which
 # forms the combined scores) and "k_select" is the rest of the selection (four launches).
 STAGES = ["k_guide_stats", "k_guide_lse", "k_quantize", "k_guide_attn", "k_sel_score", "k_select", "k_compact"]
-KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
-                  "k_guide_lse": ["guide_scores.hip", "tp_internal.h"],
-                  "k_guide_attn": ["guide_scores.hip", "tp_internal.h"],
-                  "k_guide_pool": ["guide_scores.hip", "tp_internal.h"],
+KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
+                  "k_guide_lse": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
+                  "k_guide_attn": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
+                  "k_guide_pool": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
+                  "k_guide_fwd": ["guide_attention.hip", "tile_common.h", "tp_internal.h"],
                   # the rows each step-2 launch takes are set by tp_evict
                   "k_quantize": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
                   "k_quantize_lean": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
@@ -38,7 +39,7 @@ KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tp_internal.h"],
                   "k_select": ["select.hip", "tp_internal.h", "abi.cpp"],
                   "k_compact": ["compact.hip", "tp_internal.h"],
                   "k_compact_quant": ["compact.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h"],
-                  "k_lse_import": ["guide_scores.hip", "tp_internal.h"]}
+                  "k_lse_import": ["guide_scores.hip", "tile_common.h", "tp_internal.h"]}
 
 
 def algorithmic_bytes(w, kept_total_per_head, full_codes=True, normalisers_given=False):
@@ -331,6 +332,10 @@ def main():
     ap.add_argument("--given-lse", action="store_true",
                     help="guide rows' log-normalisers supplied (as a prefill attention kernel exports them): "
                          "score pass 1 is skipped")
+    ap.add_argument("--prefill-attention", action="store_true",
+                    help="the prefill-integrated path: one step is the guide rows' prefill attention "
+                         "(tp_guide_attention over the context and the guide's own keys and values: outputs and "
+                         "normalisers) followed by tp_evict with those normalisers (a secondary line)")
     ap.add_argument("--no-full-codes", action="store_true",
                     help="step 2 writes the scales only and the compaction quantises the kept V rows "
                          "(the codes of evicted rows are never written)")
@@ -372,16 +377,28 @@ def main():
         w = w.with_(guide_lens=tuple(args.guide_tokens for _ in w.ctx_lens))
     torch.cuda.set_device(0)
     q, k, v = SD.device_inputs(w)
-    kg = SD.device_guide_keys(w) if args.guide_keys else None
+    kg = SD.device_guide_keys(w) if (args.guide_keys or args.prefill_attention) else None
+    vg = SD.device_guide_values(w) if args.prefill_attention else None
     lse = prefill_lse(w, q, k, kg) if args.given_lse else None
-    kg_arg = None if args.given_lse else kg
+    if args.prefill_attention:  # written by tp_guide_attention inside every step
+        lse = torch.empty(w.L * w.Hq * w.g_tot, dtype=torch.float32, device="cuda")
+        o_guide = torch.empty(w.L * w.Hq * w.g_tot * w.d, dtype=torch.float32, device="cuda")
+    kg_arg = None if lse is not None else kg
     d = B.dims(w.L, w.Hq, w.Hkv, w.d)
     bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
     ko = B.kept_offsets_for(bt, w.keep_ratio or 0.0, w.keep_budget or 0)
     bufs = B.EvictBuffers(d, bt, w.qfmt, w.bits, ko)
+    ws_attn = (torch.empty(B.tp_workspace_size(B.TP_FN_GUIDE_ATTENTION, d, bt), dtype=torch.uint8, device="cuda")
+               if args.prefill_attention else None)
     torch.cuda.synchronize()
 
-    def step(ev=None):
+    def step(ev=None, att=None):
+        if args.prefill_attention:
+            if att is not None:
+                att[0].record()
+            B.tp_guide_attention(d, bt, q, k, v, w.softmax_scale, o_guide, lse, ws_attn, k_guide=kg, v_guide=vg)
+            if att is not None:
+                att[1].record()
         B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
                    w.keep_budget or 0, ko, bufs.s_key, bufs.scales, None if args.no_full_codes else bufs.v_q,
                    bufs.s_comb, bufs.kept_idx, bufs.k_c,
@@ -396,15 +413,19 @@ def main():
     # data cached.  ms_per_step is the median over the K steps.
     flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.TP_EVICT_EVENTS)] for _ in range(args.steps)]
+    atts = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
         flush.fill_(i & 0xFF)
-        step(evs[i])
+        step(evs[i], atts[i])
     end.record()
     torch.cuda.synchronize()
-    step_ms = sorted(e[0].elapsed_time(e[-1]) for e in evs)
+    if args.prefill_attention:  # the step starts at the attention
+        step_ms = sorted(a[0].elapsed_time(e[-1]) for a, e in zip(atts, evs))
+    else:
+        step_ms = sorted(e[0].elapsed_time(e[-1]) for e in evs)
     ms = statistics.median(step_ms)
     stages = STAGES if lse is None else ["pass1_skipped", "k_lse_import"] + STAGES[2:]
     if args.no_full_codes:
@@ -413,6 +434,8 @@ def main():
         stages[4] = "k_guide_pool"
     stage_ms = {n: statistics.median(e[j].elapsed_time(e[j + 1]) for e in evs) for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
+    if args.prefill_attention:
+        stage_ms = dict({"k_guide_fwd": statistics.median(a[0].elapsed_time(a[1]) for a in atts)}, **stage_ms)
     timing = {"protocol": f"median of {args.steps} steps, each timed by events at its start and end on the "
                           f"stream it runs on, after {args.warmup} untimed warm-up steps; a {FLUSH_BYTES >> 20} MB "
                           f"device write before each step (outside its events) evicts the caches; stages_ms are "
@@ -426,18 +449,25 @@ def main():
     # other kernels stream HBM
     score_flops = 2 * w.L * w.Hq * sum(g * n for g, n in zip(w.guide_lens, w.ctx_lens)) * w.d
 
+    # the guide rows' attention: the score contraction and the value product (twice the flops of
+    # a score pass), over K and V once each
+    attn_flops = 2 * score_flops + (4 * w.L * w.Hq * sum(g * (g + 1) // 2 for g in w.guide_lens) * w.d
+                                    if args.prefill_attention else 0)
+    per["k_guide_fwd"] = (2 * w.L * w.Hkv * w.n_tot * w.d * 2 + w.L * w.Hq * w.g_tot * w.d * (2 + 4)
+                          + 2 * w.L * w.Hkv * w.g_tot * w.d * 2)  # K, V, Q and guide K/V read; O written
+
     def roofline_of(kern):
         # the roof is whichever of HBM bytes and matrix flops takes longer at its peak; the
         # score passes sit just below the ridge point (about 250 flop/byte against 312)
         t = stage_ms[kern] * 1e-3
         hbm = {"bound": "hbm", "achieved": round(per[kern] / t / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                "frac": round(per[kern] / t / 1e9 / HBM_PEAK_GBS, 4), "algorithmic_bytes": per[kern]}
-        if kern not in ("k_guide_stats", "k_guide_attn"):
+        if kern not in ("k_guide_stats", "k_guide_attn", "k_guide_fwd"):
             return hbm
-        mfma = {"bound": "mfma", "achieved": round(score_flops / t / 1e12, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(score_flops / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-                "flops": score_flops}
-        hbm_s, mfma_s = per[kern] / (HBM_PEAK_GBS * 1e9), score_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+        fl = attn_flops if kern == "k_guide_fwd" else score_flops
+        mfma = {"bound": "mfma", "achieved": round(fl / t / 1e12, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(fl / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4), "flops": fl}
+        hbm_s, mfma_s = per[kern] / (HBM_PEAK_GBS * 1e9), fl / (MFMA_BF16_PEAK_TFLOPS * 1e12)
         roof, other = (hbm, mfma) if hbm_s >= mfma_s else (mfma, hbm)
         return dict(roof, other_roof={k: other[k] for k in ("bound", "achieved", "unit", "frac")})
 
@@ -470,8 +500,12 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
-        "config": {"workload": w.describe() + (", guide keys in the normaliser" if kg is not None else "")
-                   + (", row normalisers supplied by the prefill (score pass 1 skipped)" if lse is not None else "")
+        "config": {"workload": w.describe()
+                   + (", the guide rows' prefill attention (context and guide keys: outputs and normalisers) "
+                      "followed by the eviction from its normalisers" if args.prefill_attention else "")
+                   + (", guide keys in the normaliser" if kg is not None and not args.prefill_attention else "")
+                   + (", row normalisers supplied by the prefill (score pass 1 skipped)"
+                      if args.given_lse else "")
                    + (", codes written for the kept rows only" if args.no_full_codes else ""),
                    "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
                    "context_tokens": w.n_tot, "guide_tokens": w.g_tot, "kept_per_head": ko[-1]},
@@ -485,7 +519,7 @@ def main():
                                  if k in ("bound", "achieved", "unit", "frac", "other_roof")}
                              for n in stage_ms if n not in ("k_guide_lse", "k_lse_import")},
     }
-    del q, k, v, kg, bufs, flush
+    del q, k, v, kg, vg, bufs, flush, ws_attn
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -74,7 +74,7 @@ enum {
 };
 
 /* Entry points that take a workspace (argument of tp_workspace_size). */
-enum { TP_FN_GUIDE_SCORES = 0, TP_FN_COMBINE_SELECT_TOPK = 1, TP_FN_EVICT = 2 };
+enum { TP_FN_GUIDE_SCORES = 0, TP_FN_COMBINE_SELECT_TOPK = 1, TP_FN_EVICT = 2, TP_FN_GUIDE_ATTENTION = 3 };
 
 typedef struct tp_dims {
   int32_t num_layers;   /* L   >= 1 */
@@ -157,6 +157,30 @@ tp_status tp_guide_scores_lse(const tp_dims* dims, const tp_batch* batch, const 
                               const void* k, const float* guide_lse, float softmax_scale,
                               int32_t pool_k, float* s_key, void* workspace, size_t ws_bytes,
                               void* stream);
+
+/*
+ * The prefill's attention for the appended guide rows (Sec. 3.2: the guide follows the
+ * context and attends causally), whose normalisers feed step 1 (tp_guide_scores_lse,
+ * tp_evict's guide_lse), so the eviction adds one sweep over K to this one:
+ *   x_jt = softmax_scale * <q_guide[l][r][g0+j], key_t> over the keys row j sees: the N_b
+ *          context keys k[l][h][n0+i], and, when k_guide is given, the guide keys
+ *          k_guide[l][h][g0+t] for t <= j;
+ *   o_guide[l][r][g0+j][:] = sum_t exp(x_jt) value_t / sum_t exp(x_jt)   (values v, v_guide),
+ *   guide_lse[l][r][g0+j]  = ln sum_t exp(x_jt),
+ * for query head r of KV head h = r / (Hq/Hkv) and every guide token j of sequence b.
+ * q_guide bf16 [L][Hq][G_tot][d]; k, v bf16 [L][Hkv][N_tot][d]; k_guide, v_guide bf16
+ * [L][Hkv][G_tot][d], both NULL (the context only) or both given; o_guide fp32
+ * [L][Hq][G_tot][d] (out); guide_lse fp32 [L][Hq][G_tot] (out).  softmax_scale > 0.
+ * workspace: device, >= tp_workspace_size(TP_FN_GUIDE_ATTENTION, ...) bytes, 256-byte
+ * aligned (per chunk of context tokens and guide row, a partial maximum, sum and output).
+ * The probabilities are rounded to bf16 for the value product (as flash attention does);
+ * the normalisers are fp32 sums of the unrounded ones.
+ * Errors: TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE,
+ * TP_ERR_HIP.
+ */
+tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                             const void* v, const void* k_guide, const void* v_guide, float softmax_scale,
+                             float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Step 2 — value score of Eq. 2 (Sec. 3.3), fused with per-token quantisation of V

@@ -17,12 +17,13 @@ LIB_PATH = os.path.join(_HERE, "lib", "libtaskpress.so")
 TP_OK, TP_ERR_NULL, TP_ERR_SHAPE, TP_ERR_PARAM, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE, TP_ERR_HIP = range(7)
 TP_QFMT_INT, TP_QFMT_FP8_E4M3 = 0, 1
 TP_COMBINE_MUL, TP_COMBINE_NORM_ADD, TP_COMBINE_HARMONIC, TP_COMBINE_KEY_ONLY = 0, 1, 2, 3
-TP_FN_GUIDE_SCORES, TP_FN_COMBINE_SELECT_TOPK, TP_FN_EVICT = 0, 1, 2
+TP_FN_GUIDE_SCORES, TP_FN_COMBINE_SELECT_TOPK, TP_FN_EVICT, TP_FN_GUIDE_ATTENTION = 0, 1, 2, 3
 TP_MAX_BATCH = 64
 TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
-            "tp_guide_scores", "tp_guide_scores_lse", "tp_quantize_v_scales", "tp_combine_select_topk",
+            "tp_guide_scores", "tp_guide_scores_lse", "tp_guide_attention", "tp_quantize_v_scales",
+            "tp_combine_select_topk",
             "tp_combine_select_topk_static", "tp_compact_kv", "tp_compact_quantize_kv", "tp_evict")
 TP_STATIC_SCRATCH_BYTES = 64 << 20
 
@@ -112,6 +113,8 @@ def load():
     lib.tp_guide_scores.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
     lib.tp_guide_scores_lse.restype = ctypes.c_int32
     lib.tp_guide_scores_lse.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
+    lib.tp_guide_attention.restype = ctypes.c_int32
+    lib.tp_guide_attention.argtypes = [pd, pb, P, P, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
     lib.tp_quantize_v_scales.restype = ctypes.c_int32
     lib.tp_quantize_v_scales.argtypes = [pd, pb, P, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.tp_combine_select_topk.restype = ctypes.c_int32
@@ -209,6 +212,27 @@ def tp_guide_scores_lse(d: TpDims, batch: Batch, q_guide, k, guide_lse, softmax_
     _check(load().tp_guide_scores_lse(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k),
                                       _ptr(guide_lse), float(softmax_scale), int(pool_k), _ptr(s_key),
                                       _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def tp_guide_attention(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, o_guide, guide_lse,
+                       workspace=None, stream=None, k_guide=None, v_guide=None):
+    """The prefill's attention for the appended guide rows: o_guide fp32 [L][Hq][G_tot][d] and
+    guide_lse fp32 [L][Hq][G_tot] (natural log), over the context and, with k_guide / v_guide
+    bf16 [L][Hkv][G_tot][d], the guide keys 0..j of each row j."""
+    L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
+    _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(v, L * Hkv * batch.n_tot * D * 2, "v")
+    _need(k_guide, L * Hkv * batch.g_tot * D * 2, "k_guide")
+    _need(v_guide, L * Hkv * batch.g_tot * D * 2, "v_guide")
+    _need(o_guide, L * Hq * batch.g_tot * D * 4, "o_guide")
+    _need(guide_lse, L * Hq * batch.g_tot * 4, "guide_lse")
+    if workspace is None:
+        workspace = torch.empty(tp_workspace_size(TP_FN_GUIDE_ATTENTION, d, batch), dtype=torch.uint8,
+                                device=q_guide.device)
+    _check(load().tp_guide_attention(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(v),
+                                     _ptr(k_guide), _ptr(v_guide), float(softmax_scale), _ptr(o_guide),
+                                     _ptr(guide_lse), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def row_bytes(qfmt: int, bits: int, head_dim: int) -> int:

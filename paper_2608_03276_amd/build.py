@@ -26,7 +26,7 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"),
 ]
-SOURCES = ["abi.cpp", "guide_scores.hip", "quantize.hip", "select.hip", "compact.hip"]
+SOURCES = ["abi.cpp", "guide_scores.hip", "guide_attention.hip", "quantize.hip", "select.hip", "compact.hip"]
 # The score passes see finite inputs only (the ABI's precondition; -inf marks masked logits),
 # so max() need not quiet NaNs: this drops the canonicalising moves before every v_max.
 EXTRA_FLAGS = {"guide_scores.hip": ["-fno-honor-nans"]}

@@ -460,6 +460,14 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
     *bytes = select_workspace(dims, batch);
     return ok();
   }
+  if (fn == TP_FN_GUIDE_ATTENTION) {
+    s = check_batch(batch, true);
+    if (s != TP_OK) return s;
+    *bytes = tp::attn_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads, dims->head_dim,
+                                       batch->ctx_offsets, batch->guide_offsets, batch->batch)
+                 .total;
+    return ok();
+  }
   if (fn == TP_FN_EVICT) {
     s = check_batch(batch, true);
     if (s != TP_OK) return s;
@@ -491,6 +499,66 @@ tp_status tp_guide_scores_lse(const tp_dims* dims, const tp_batch* batch, const 
   if (s != TP_OK) return s;
   const hipError_t e = tp::launch_guide_scores(a, dims->head_dim, (hipStream_t)stream, nullptr);
   if (e != hipSuccess) return hip_fail(e, "tp_guide_scores_lse launch");
+  return ok();
+}
+
+tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                             const void* v, const void* k_guide, const void* v_guide, float softmax_scale,
+                             float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream) {
+  tp_status s = check_dims(dims);
+  if (s != TP_OK) return s;
+  s = check_batch(batch, true);
+  if (s != TP_OK) return s;
+  if (!q_guide || !k || !v || !o_guide || !guide_lse)
+    return fail(TP_ERR_NULL, "q_guide, k, v, o_guide and guide_lse must be non-NULL");
+  if ((k_guide == nullptr) != (v_guide == nullptr))
+    return fail(TP_ERR_NULL, "k_guide and v_guide must both be given or both NULL");
+  if (!aligned16(q_guide) || !aligned16(k) || !aligned16(v) || !aligned16(o_guide) ||
+      (k_guide && (!aligned16(k_guide) || !aligned16(v_guide))))
+    return fail(TP_ERR_PARAM, "tensor pointers must be 16-byte aligned");
+  if (((uintptr_t)guide_lse & 3u) != 0) return fail(TP_ERR_PARAM, "guide_lse must be 4-byte aligned");
+  if (!(softmax_scale > 0.0f) || !isfinite(softmax_scale))
+    return fail(TP_ERR_PARAM, "softmax_scale must be finite and > 0");
+  const tp::AttnWorkspace lay = tp::attn_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads,
+                                                          dims->head_dim, batch->ctx_offsets, batch->guide_offsets,
+                                                          batch->batch);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TP_ERR_WORKSPACE, "workspace needs %zu bytes (got %zu%s)", lay.total, ws_bytes,
+                workspace ? "" : ", NULL");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(TP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  tp::AttnArgs a;
+  memset(&a, 0, sizeof a);
+  a.bt = batch_args(batch, true);
+  a.q = (const uint16_t*)q_guide;
+  a.k = (const uint16_t*)k;
+  a.v = (const uint16_t*)v;
+  a.kg = (const uint16_t*)k_guide;
+  a.vg = (const uint16_t*)v_guide;
+  a.o = o_guide;
+  a.lse = guide_lse;
+  a.pstat = (float2*)((char*)workspace + lay.pstat_off);
+  a.po = (float*)((char*)workspace + lay.po_off);
+  a.L = dims->num_layers;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.R = dims->num_q_heads / dims->num_kv_heads;
+  a.n_tot = batch->ctx_offsets[batch->batch];
+  a.g_tot = batch->guide_offsets[batch->batch];
+  a.c = (float)((double)softmax_scale * 1.4426950408889634);
+  a.chunk = tp::attn_chunk_tokens(batch->ctx_offsets, batch->batch);
+  int64_t max_nb = 0, max_gb = 0;
+  for (int b = 0; b < batch->batch; ++b) {
+    max_nb = std::max<int64_t>(max_nb, batch->ctx_offsets[b + 1] - batch->ctx_offsets[b]);
+    max_gb = std::max<int64_t>(max_gb, batch->guide_offsets[b + 1] - batch->guide_offsets[b]);
+  }
+  const int64_t nchunk = (max_nb + a.chunk - 1) / a.chunk;
+  const int64_t nrg = (a.R * max_gb + tp::kRowsPerGroup - 1) / tp::kRowsPerGroup;
+  if (nchunk + 1 > 0x7FFFFFFF || (int64_t)batch->batch * nrg > 65535)
+    return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
+  a.nchunk_max = (int32_t)nchunk;
+  a.nrg_max = (int32_t)nrg;
+  const hipError_t e = tp::launch_guide_attention(a, dims->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tp_guide_attention launch");
   return ok();
 }
 

@@ -23,29 +23,11 @@
 // barrier is needed inside the main loop and the K fragments take no prefetch registers.
 // Inside a sub-tile the wave is software-pipelined: the MFMAs of one pair of 32-row blocks
 // run while the vector ALU does the softmax work of the previous pair.
+#include "tile_common.h"
 #include "tp_internal.h"
 
 namespace tp {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-union Frag {
-  uint4 u;
-  bf16x8 v;
-};
-
-template <int D>
-struct Cfg {
-  static constexpr int kSteps = D / 16;                  // MFMA k-steps over d
-  static constexpr int kPieces = D / 8;                  // 16-byte pieces per row
-  static constexpr int kRowBytes = D * 2;
-  static constexpr int kStride = kRowBytes + 16;         // LDS bytes per staged query row
-  static constexpr int kStageBytes = 32 * kRowBytes;     // one K sub-tile
-  static constexpr int kTokPerKB = 1024 / kRowBytes;     // tokens per 1 KB copy instruction
-};
 
 struct Work {
   int b, seg, l, h, rg, chunk;
@@ -53,7 +35,6 @@ struct Work {
   int gb, rows, row0, nrows;
 };
 
-__device__ inline int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Workgroup -> (sequence, row group, chunk, segment).  Each sequence owns a contiguous range
 // of workgroup ids (wg_off).  Within it the work units (segment, chunk) are numbered
@@ -120,15 +101,6 @@ __device__ inline void read_qfrag(const char* qs, int rb, Frag (&qf)[Cfg<D>::kSt
   for (int s = 0; s < C::kSteps; ++s) qf[s].u = *(const uint4*)(base + 16 * s);
 }
 
-// K sub-tiles in a wave's LDS staging buffer: token tl (0..31) of the sub-tile at
-// tl * kRowBytes, its 16-byte piece p stored in slot p ^ swz(tl).  The swizzle puts the 16
-// (D = 128) or 8 (D = 64, two rows per 256 bytes) tokens read by one group of lanes on
-// different banks.
-template <int D>
-__device__ inline int swz(int tl) {
-  return D == 128 ? (tl & 15) : ((tl >> 1) & 7);
-}
-
 // Issue the copy of the sub-tile starting at chunk token t0 into `kbuf`: each instruction
 // moves 1 KB of consecutive K rows (coalesced); lane i fills slot i of that kilobyte, so it
 // fetches the piece that the swizzle assigns to that slot.  Tokens past the chunk's `ntok`
@@ -145,20 +117,6 @@ __device__ inline void dma_subtile(const char* kchunk, int t0, int ntok, char* k
     const char* src = kchunk + (uint32_t)tok * C::kRowBytes + p * 16;
     __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(kbuf + j * 1024), 16,
                                      0, 0);
-  }
-}
-
-// K fragment of the staged sub-tile: token lane%32, the d-columns of this half-wave.
-template <int D>
-__device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) {
-  using C = Cfg<D>;
-  const int lane = threadIdx.x & 63;
-  const int tl = lane & 31;
-  const char* row = kbuf + tl * C::kRowBytes;
-#pragma unroll
-  for (int s = 0; s < C::kSteps; ++s) {
-    const int p = (lane >> 5) * (C::kPieces / 2) + s;
-    kf[s].u = *(const uint4*)(row + ((p ^ swz<D>(tl)) * 16));
   }
 }
 
@@ -229,17 +187,6 @@ __device__ inline void step_schedule() {
 // Keeps the vector work of a pipeline step inside the step: without a use here the
 // compiler sinks it past the loop's branches, away from the MFMAs it should overlap.
 __device__ inline void pin(float a, float b, float c, float d) { asm volatile("" ::"v"(a), "v"(b), "v"(c), "v"(d)); }
-
-// Running (max, sum) statistics start at (-FLT_MAX, 0) rather than (-inf, 0): merging a
-// unit whose logits are all -inf (masked tokens, or the empty pipeline slot before the
-// first pair) is then an exact no-op, with no special case.
-constexpr float kNoMax = -3.402823466e38f;
-
-__device__ inline void merge_stats(float& m, float& s, float m2, float s2) {
-  const float mn = fmaxf(m, m2);
-  s = s * __builtin_amdgcn_exp2f(m - mn) + s2 * __builtin_amdgcn_exp2f(m2 - mn);
-  m = mn;
-}
 
 __device__ inline float max16(const f32x16& x) {
   const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);

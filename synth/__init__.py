@@ -16,7 +16,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
-TAG_Q, TAG_K, TAG_V, TAG_KG = 1, 2, 3, 5  # TAG_KG: keys of the guide tokens
+TAG_Q, TAG_K, TAG_V, TAG_KG, TAG_VG = 1, 2, 3, 5, 6  # TAG_KG / TAG_VG: keys / values of the guide tokens
 DIST_NORMAL, DIST_STUDENT_T3 = 0, 1
 
 

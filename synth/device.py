@@ -5,7 +5,7 @@ from __future__ import annotations
 
 import torch
 
-from . import TAG_KG, Stream, device_fill
+from . import TAG_KG, TAG_VG, Stream, device_fill
 
 
 def device_inputs(w, device="cuda"):
@@ -33,3 +33,16 @@ def device_guide_keys(w, device="cuda"):
     device_fill(kg.data_ptr(), guide_key_stream(w), w.L, w.Hkv, list(w.guide_lens), w.d,
                 torch.cuda.current_stream().cuda_stream)
     return kg
+
+
+def guide_value_stream(w):
+    """The guide tokens' values of workload w (N(0,1), same seed as its guide queries)."""
+    return Stream(w.q.seed, TAG_VG)
+
+
+def device_guide_values(w, device="cuda"):
+    """v_guide bf16 [L][Hkv][G_tot][d] of workload w."""
+    vg = torch.empty(w.L * w.Hkv * w.g_tot * w.d, dtype=torch.bfloat16, device=device)
+    device_fill(vg.data_ptr(), guide_value_stream(w), w.L, w.Hkv, list(w.guide_lens), w.d,
+                torch.cuda.current_stream().cuda_stream)
+    return vg

@@ -43,7 +43,7 @@
 
 #define SYN_GAMMA 0x9E3779B97F4A7C15ULL
 
-enum { SYN_TAG_Q = 1, SYN_TAG_K = 2, SYN_TAG_V = 3, SYN_TAG_OUTLIER = 4, SYN_TAG_KG = 5 };
+enum { SYN_TAG_Q = 1, SYN_TAG_K = 2, SYN_TAG_V = 3, SYN_TAG_OUTLIER = 4, SYN_TAG_KG = 5, SYN_TAG_VG = 6 };
 enum { SYN_DIST_NORMAL = 0, SYN_DIST_STUDENT_T3 = 1 };
 
 SYN_FN uint64_t syn_mix(uint64_t z) {
@@ -231,7 +231,7 @@ SYN_FN uint64_t syn_outlier_count(double frac, uint64_t n) {
 
 typedef struct syn_spec {
   uint64_t seed;
-  int32_t tag;       /* SYN_TAG_Q / K / V / KG (the guide tokens' keys) */
+  int32_t tag;       /* SYN_TAG_Q / K / V / KG / VG (the guide tokens' keys and values) */
   int32_t dist;      /* SYN_DIST_* */
   double out_frac;   /* fraction of tokens per (seq, layer, head) that are outliers; 0 = none */
   double out_scale;  /* factor applied to outlier rows before the bf16 rounding */

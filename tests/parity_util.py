@@ -16,7 +16,8 @@ import torch
 
 import synth
 from oracle import taskpress_oracle as o
-from synth.device import device_guide_keys, device_inputs, guide_key_stream  # noqa: F401 (re-exported)
+from synth.device import (device_guide_keys, device_guide_values, device_inputs, guide_key_stream,  # noqa: F401
+                          guide_value_stream)
 from paper_2608_03276_amd import binding as B
 
 RTOL = 1e-3
@@ -30,6 +31,11 @@ def log(msg):
 def host_guide_keys(w, b, l, h):
     """bf16 bits of the guide keys of segment (b, l, h): [G_b, d]."""
     return synth.rows(guide_key_stream(w), b, l, h, w.guide_lens[b], w.d)
+
+
+def host_guide_values(w, b, l, h):
+    """bf16 bits of the guide values of segment (b, l, h): [G_b, d]."""
+    return synth.rows(guide_value_stream(w), b, l, h, w.guide_lens[b], w.d)
 
 
 def host_segment(w, b, l, h):

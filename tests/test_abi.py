@@ -209,6 +209,31 @@ def test_select_static_validation():
 
 
 @no_gpu
+def test_guide_attention_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300], [0, 16, 20])
+    ws = B.tp_workspace_size(B.TP_FN_GUIDE_ATTENTION, d, bt)
+    # at least a partial (max, sum) and output per guide row and slot (one chunk and the guide keys)
+    assert ws >= 2 * 8 * 20 * 2 * (8 + 64 * 4)
+
+    def att(q=FAKE, k=FAKE, v=FAKE, kg=None, vg=None, scale=0.125, o_=FAKE, lse=FAKE, w=FAKE, wsb=ws, batch=bt):
+        return lib.tp_guide_attention(ctypes.byref(d), ctypes.byref(batch.c), q, k, v, kg, vg, scale, o_, lse, w,
+                                      wsb, None)
+
+    assert att(v=None) == B.TP_ERR_NULL
+    assert att(lse=None) == B.TP_ERR_NULL
+    assert att(kg=FAKE) == B.TP_ERR_NULL        # guide keys without their values
+    assert att(vg=FAKE) == B.TP_ERR_NULL
+    assert att(o_=FAKE + 4) == B.TP_ERR_PARAM   # not 16-byte aligned
+    assert att(lse=FAKE + 2) == B.TP_ERR_PARAM
+    assert att(scale=0.0) == B.TP_ERR_PARAM
+    assert att(w=None) == B.TP_ERR_WORKSPACE
+    assert att(wsb=ws - 1) == B.TP_ERR_WORKSPACE
+    assert att(w=FAKE + 16) == B.TP_ERR_WORKSPACE
+    assert att(batch=B.Batch([0, 100, 300])) == B.TP_ERR_NULL  # guide offsets required
+
+
+@no_gpu
 def test_compact_validation():
     d = B.dims(2, 8, 2, 64)
     bt = B.Batch([0, 100, 300])
