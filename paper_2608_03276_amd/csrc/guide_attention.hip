@@ -6,18 +6,20 @@
 // needs one more sweep over K on top of this one instead of two.
 //
 // Flash-attention style, split over the context in chunks: one workgroup per (sequence,
-// layer, KV head, chunk, group of <= 256 guide rows), eight waves, wave w owning 32 rows.  Per
-// 32-token sub-tile, shared by the waves through LDS (double-buffered, one barrier per
-// sub-tile):
-//   S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (tokens on M, rows on N), so a lane holds one row
-//       and 16 tokens (the score passes' pass-1 layout) and the row's running maximum and sum
-//       stay in the lane (and its partner lane 32 apart, which holds the other 16 tokens);
-//   P  = exp2(S c - m), m raised only when a logit exceeds it by more than kLazyRaise (the
-//       maximum needs only to be a logit already seen, so rescaling O is rare);
-//   O^T += V^T P^T on the same instruction (d on M, rows on N): the B operand is the lane's own
-//       16 probabilities in bf16, the contraction index mapped to exactly the tokens the lane
-//       holds, and the A operand reads V transposed from LDS, where each sub-tile is staged
-//       d-major.
+// layer, KV head, chunk, group of <= 256 guide rows), eight waves (two per SIMD, so that one
+// wave's exponentials overlap the other's MFMAs), wave w owning rows 32w .. 32w + 31.  The
+// chunk's 32-token sub-tiles of K and V stream through a ring of LDS slots filled by direct
+// global->LDS copies issued several sub-tiles ahead (one barrier per sub-tile), and every
+// wave reads the whole sub-tile.  Per sub-tile, on v_mfma_f32_32x32x16_bf16:
+//   S^T = K Q^T (tokens on M, rows on N): a lane holds one row and 16 of the 32 tokens (its
+//       partner lane 32 apart holds the other 16), so the row's running maximum and sum stay
+//       in the lane pair;
+//   P  = exp2(S c - m) against the pair's current maximum m, which is raised (with O and the
+//       sum rescaled) only when a lane's 16 terms would sum past 2^32; m is always a logit
+//       already seen, which is all the normaliser needs;
+//   O^T += V^T P^T (d on M, rows on N): the B operand is the lane's own 16 probabilities in
+//       bf16, the contraction index mapped to exactly the tokens the lane holds; the A
+//       operand comes from the token-major V sub-tile through transposing LDS reads.
 // Each workgroup writes its rows' partial (max, sum) and unnormalised O; the guide's own keys
 // are one more chunk, with the causal mask.  A merge kernel combines the chunks.
 #include "tile_common.h"
@@ -26,71 +28,153 @@
 namespace tp {
 namespace {
 
-constexpr int kAttnThreads = 512;  // 8 waves, one per 32-row block of a row group
+constexpr int kAttnThreads = 512;  // 8 waves, two per SIMD, 32 rows each
 constexpr int kAttnWaves = kAttnThreads / 64;
-constexpr float kLazyRaise = 8.0f;  // log2 units: probabilities stay below 2^8 between raises
-constexpr int kVtStride = 64;       // bytes per d-row of a transposed V sub-tile (32 tokens)
+constexpr float kAttnLazyLimit = 4294967296.0f;  // 2^32: a lane's 16 terms against a stale maximum
 
-// Byte offset of token tk of d-row d in a transposed V sub-tile: groups of 4 tokens (8 bytes)
-// are permuted within the row by d/8, so the 16 d-rows written together by one load of
-// 8 d-values per thread do not all land on one bank.
-__device__ inline int vt_off(int d, int tk) {
-  return d * kVtStride + ((((tk >> 2) ^ (d >> 3)) & 7) << 3) + ((tk & 3) << 1);
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct AttnCfg {
+  static constexpr int kTileBytes = 32 * D * 2;                // one 32-token K (or V) sub-tile
+  static constexpr int kSlotBytes = 2 * kTileBytes;            // a ring slot: K, then V
+  static constexpr int kCopies = kSlotBytes / 1024 / kAttnWaves;  // 1 KB copies per wave per sub-tile
+  static constexpr int kRing = D == 128 ? 9 : 16;             // slots: 144 KB / 128 KB of LDS
+  static_assert(kRing * kSlotBytes <= 160 * 1024, "LDS of one CU");
+  static_assert(kRing - 4 <= 12 && (kRing - 4) * kCopies <= 63, "wait_copies_but cases and the vmcnt range");
+};
+
+// V sub-tiles are staged like K (16-byte piece p of token tl in slot p ^ swzv(tl)) with their
+// own permutation, chosen for the transposing reads: a half-wave reads 4 consecutive tokens,
+// 4 pieces each (16 lanes: 2 pieces each), and swzv gives the 4 tokens disjoint bank sets in
+// both groupings (a 256-byte row covers every bank of the 64).
+template <int D>
+__device__ inline int swzv(int tl) {
+  if (D == 128) return (0xCA60 >> (4 * (tl & 3))) & 15;  // 0, 6, 10, 12
+  return 2 * (tl & 3);
 }
 
-// Issue the copy of K sub-tile rows [t0, t0 + 32) of `ksrc` (rows past ntok repeat its last
-// row) into `kbuf` in the score passes' staged layout: the kilobyte pieces go to the first
-// waves, one each, so the whole workgroup shares the tile.
+// One global->LDS copy of 16 bytes per lane: lane i's bytes from src land at LDS byte
+// lds + 16 i.  Inline assembly rather than the builtin, because the compiler cannot tell the
+// ring's slots apart and would drain every copy in flight before each LDS read of the ring;
+// completion is tracked by the explicit vmcnt waits below instead.  One wait state separates
+// the M0 write from the copy that reads it.
+__device__ inline void copy16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+
+// Issue this wave's share of the copies of sub-tile rows [t0, t0 + 32) of K and V into the
+// slot at LDS byte `slot` (rows past ntok repeat the last row: finite data the masks drop).
+// The 2 * kTileBytes / 1 KB copies go kCopies to a wave: K's first, then V's.
 template <int D>
-__device__ inline void stage_k(const char* ksrc, int t0, int ntok, char* kbuf, int wave) {
+__device__ inline void copy_subtile(const char* kbase, const char* vbase, int t0, int ntok, uint32_t slot, int wave) {
   using C = Cfg<D>;
-  constexpr int kKBs = 32 / C::kTokPerKB;
-  if (wave >= kKBs) return;
+  constexpr int kKB = 32 / C::kTokPerKB;  // 1 KB copies per 32-token tile
   const int lane = threadIdx.x & 63;
-  const int tl = wave * C::kTokPerKB + lane / C::kPieces;
-  const int p = (lane % C::kPieces) ^ swz<D>(tl);
-  const int tok = min(t0 + tl, ntok - 1);
-  const char* src = ksrc + (uint32_t)tok * C::kRowBytes + p * 16;
-  __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(kbuf + wave * 1024), 16,
-                                   0, 0);
-}
-
-// Thread t of the first 32 * D/8 threads holds 16 bytes (d-values 8p .. 8p+7 of token tk) of
-// a V sub-tile: loaded here, written transposed by write_vt.
-template <int D>
-__device__ inline uint4 load_v(const uint16_t* vsrc, int t0, int ntok) {
-  constexpr int kPieces = D / 8;
-  const int tid = threadIdx.x;
-  if (tid >= 32 * kPieces) return make_uint4(0, 0, 0, 0);
-  const int tk = tid / kPieces, p = tid % kPieces;
-  const int tok = min(t0 + tk, ntok - 1);
-  return *(const uint4*)(vsrc + (int64_t)tok * D + p * 8);
-}
-
-template <int D>
-__device__ inline void write_vt(char* vt, const uint4& x) {
-  constexpr int kPieces = D / 8;
-  const int tid = threadIdx.x;
-  if (tid >= 32 * kPieces) return;
-  const int tk = tid / kPieces, d0 = (tid % kPieces) * 8;
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-  for (int e = 0; e < 8; ++e)
-    *(uint16_t*)(vt + vt_off(d0 + e, tk)) = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+  for (int i = 0; i < AttnCfg<D>::kCopies; ++i) {
+    const int j = wave * AttnCfg<D>::kCopies + i;  // wave-uniform
+    const bool isv = j >= kKB;
+    const int jj = isv ? j - kKB : j;
+    const int tl = jj * C::kTokPerKB + lane / C::kPieces;
+    const int p = (lane % C::kPieces) ^ (isv ? swzv<D>(tl) : swz<D>(tl));
+    const int tok = min(t0 + tl, ntok - 1);
+    copy16((isv ? vbase : kbase) + (uint32_t)tok * C::kRowBytes + p * 16, slot + (uint32_t)j * 1024u);
+  }
 }
 
-// A operand of O^T += V^T P^T for k-step s2 and d-block db: V^T[d][k] with d = 32 db + lane%32
-// and the contraction index k = 8 (lane/32) + j standing for token 16 s2 + 8 (j/4) +
-// 4 (lane/32) + j%4, the tokens whose probabilities the lane holds (acc[8 s2 + j]).
-__device__ inline Frag read_vfrag(const char* vt, int db, int s2) {
+// Wait until at most k sub-tiles' copies of this wave are still in flight (copies complete in
+// issue order).  k is wave-uniform and at most kRing - 4 (12).
+template <int PER>
+__device__ inline void wait_copies_but(int k) {
+  switch (k) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(PER) : "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER) : "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * PER) : "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * PER) : "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(5 * PER) : "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * PER) : "memory"); break;
+    case 7: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(7 * PER) : "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(8 * PER) : "memory"); break;
+    case 9: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(9 * PER) : "memory"); break;
+    case 10: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(10 * PER) : "memory"); break;
+    case 11: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(11 * PER) : "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(12 * PER) : "memory"); break;
+  }
+}
+
+// Every wave's copies up to the waited point have landed and every wave's LDS reads before
+// this point are complete: the barrier without the full memory fence of __syncthreads, which
+// would also drain the copies still in flight.  The LDS wait is the builtin (vmcnt and expcnt
+// left at their maxima, lgkmcnt 0), which the compiler sees: it then knows the fragments read
+// before the barrier have arrived and adds no wait of its own for them after it.
+__device__ inline void ring_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A operand of O^T += V^T P^T for d-block db and k-step s2, from the token-major V sub-tile:
+// lane l needs V^T[d][k] for d = 32 db + l%32 and k = 8 (l/32) + e, e = 0..7, standing for
+// token 16 s2 + 8 (e/4) + 4 (l/32) + e%4 (the tokens whose probabilities the lane holds).
+// A transposing read hands lane i of each 16-lane group element e from the 8 bytes that lane
+// 4e + i/4 of the group addressed, element i%4; so source lane s addresses the 4 d-values
+// 32 db + 16 ((l/16)%2) + 4 (s%4) .. +3 of token 16 s2 + 8 call + 4 (l/32) + s/4.
+template <int D>
+__device__ inline Frag read_vfrag(const char* vtile, int db, int s2) {
+  using C = Cfg<D>;
   const int lane = threadIdx.x & 63;
-  const int d = 32 * db + (lane & 31);
-  const int h = lane >> 5;
+  const int h = lane >> 5, g = (lane >> 4) & 1, s = lane & 15;
+  const int col = 32 * db + 16 * g + 4 * (s & 3);  // first d-value addressed
+  union {
+    v4i16 v;
+    uint2 u;
+  } r[2];
+#pragma unroll
+  for (int call = 0; call < 2; ++call) {
+    const int tl = 16 * s2 + 8 * call + 4 * h + (s >> 2);
+    const char* addr = vtile + tl * C::kRowBytes + (((col >> 3) ^ swzv<D>(tl)) << 4) + ((col & 7) << 1);
+    r[call].v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)addr);
+  }
   Frag f;
-  const uint2 lo = *(const uint2*)(vt + vt_off(d, 16 * s2 + 4 * h));
-  const uint2 hi = *(const uint2*)(vt + vt_off(d, 16 * s2 + 8 + 4 * h));
-  f.u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  f.u = make_uint4(r[0].u.x, r[0].u.y, r[1].u.x, r[1].u.y);
   return f;
+}
+
+__device__ inline float max16(const f32x16& x) {
+  const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
+  const float a2 = fmaxf(fmaxf(x[6], x[7]), x[8]), a3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
+  const float a4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
+  return fmaxf(fmaxf(fmaxf(a0, a1), x[15]), fmaxf(fmaxf(a2, a3), a4));
+}
+
+__device__ inline float terms(const f32x16& s, float c, float m, float (&p)[16]) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(fmaf(s[i], c, -m));
+  float e[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) e[j] = (p[j] + p[4 + j]) + (p[8 + j] + p[12 + j]);
+  return (e[0] + e[1]) + (e[2] + e[3]);
+}
+
+// The rare exact update of the lane pair's maximum (a row's first sub-tile, or a logit more
+// than about 32 above its maximum in log2 units): m raised to the sub-tile's maximum, the sum
+// and the output rescaled, the terms recomputed.  Both lanes of a row take it together.
+template <int NDB>
+__device__ inline void raise_max(const f32x16& s, float c, float& m, float& l, f32x16 (&ot)[NDB], float (&p)[16],
+                                 float& ps) {
+  float mx = max16(s) * c;  // c > 0
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mn = fmaxf(m, mx);
+  const float al = __builtin_amdgcn_exp2f(m - mn);
+  l *= al;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) ot[db][i] *= al;
+  m = mn;
+  ps = terms(s, c, m, p);
 }
 
 struct AttnUnit {
@@ -137,20 +221,22 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   AttnUnit u;
   if (!attn_unit(a, u)) return;
   using C = Cfg<D>;
+  using AC = AttnCfg<D>;
   constexpr int KS = C::kSteps;
   constexpr int NDB = D / 32;  // 32-wide d-blocks of O
-  __shared__ __attribute__((aligned(1024))) char kst[2][C::kStageBytes];
-  __shared__ __attribute__((aligned(16))) char vts[2][D * kVtStride];
+  constexpr int RING = AC::kRing;
+  __shared__ __attribute__((aligned(1024))) char ring[RING * AC::kSlotBytes];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const bool active = 32 * wave < u.nrows;
-  // this lane's guide row (rows past the group's end repeat its last row; never written)
+  // this lane's guide row (rows past the group's end repeat its last row and are never
+  // written)
   const int rho_raw = u.row0 + 32 * wave + (lane & 31);
   const bool row_ok = rho_raw < u.row0 + u.nrows;
   const int rho = row_ok ? rho_raw : u.row0 + u.nrows - 1;
-  const int r = rho / u.gb, j = rho % u.gb;
-  const int64_t grow = ((int64_t)u.l * a.Hq + (int64_t)u.h * a.R + r) * a.g_tot + u.g0 + j;
-  // the K fragments' contraction order: half-wave h holds d-columns h D/2 + 8 s .. + 8 at k-step s
+  const int r = rho / u.gb, jrow = rho % u.gb;
+  const int64_t grow = ((int64_t)u.l * a.Hq + (int64_t)u.h * a.R + r) * a.g_tot + u.g0 + jrow;
+  // the K fragments' contraction order: half-wave h holds d-columns h D/2 + 8 s .. + 8
   Frag qf[KS];
 #pragma unroll
   for (int s = 0; s < KS; ++s) qf[s].u = *(const uint4*)(a.q + grow * D + (lane >> 5) * (D / 2) + 8 * s);
@@ -163,75 +249,126 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     ksrc = a.k + ((int64_t)u.seg * a.n_tot + u.n0 + (int64_t)u.chunk * a.chunk) * D;
     vsrc = a.v + ((int64_t)u.seg * a.n_tot + u.n0 + (int64_t)u.chunk * a.chunk) * D;
   }
-  const int nsub = (u.ntok + 31) / 32;
+  const char* kb = (const char*)ksrc;
+  const char* vb = (const char*)vsrc;
+  const int ntok = u.ntok;
+  const int nsub = (ntok + 31) / 32;
 
   float m = kNoMax, lsum = 0.f;
   f32x16 ot[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) ot[db] = (f32x16){};
 
-  stage_k<D>((const char*)ksrc, 0, u.ntok, kst[0], wave);
-  write_vt<D>(vts[0], load_v<D>(vsrc, 0, u.ntok));
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
+  // The query loads complete here, in a wait the compiler knows of: it then has no load of
+  // its own in flight inside the loop and inserts no waits there (which, blind to the ring's
+  // copies, would drain them).
+  __builtin_amdgcn_s_waitcnt(0);
+  const uint32_t ring_lds = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uintptr_t)(__attribute__((address_space(3))) char*)ring);
+  // Software pipeline: iteration t issues, interleaved with the exponentials of sub-tile t,
+  // the MFMAs of S for sub-tile t + 1 and of O += V P for sub-tile t - 1 (neither depends on
+  // those exponentials, so the matrix pipe has work while the vector ALU computes them); then
+  // it reads the V fragments of sub-tile t and the K fragments of sub-tile t + 2, so every
+  // operand of the next iteration is in registers when it starts.  A raise of the maximum in
+  // iteration t rescales O after sub-tile t - 1 has been added with the old maximum.  The
+  // copies run RING - 1 sub-tiles ahead; the barrier closing iteration t follows the landing
+  // of sub-tile t + 3.
+  // prologue: sub-tiles 0 .. RING-2 in flight; 0, 1 and 2 landed before the loop
+  for (int t = 0; t < RING - 1 && t < nsub; ++t)
+    copy_subtile<D>(kb, vb, 32 * t, ntok, ring_lds + (uint32_t)(t * AC::kSlotBytes), wave);
+  wait_copies_but<AC::kCopies>(max(min(RING - 2, nsub - 1) - 2, 0));
+  ring_barrier();
+  Frag kf[KS];
+  Frag vf[NDB][2];  // V of the sub-tile whose O += V P is pending (zero before the first)
+  bf16x8 pb[2];     // its probabilities
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) vf[db][0].u = vf[db][1].u = make_uint4(0, 0, 0, 0);
+  pb[0] = pb[1] = (bf16x8){};
+  f32x16 sc = {};
+  if (active) {
+    read_kfrag<D>(ring, kf);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, sc, 0, 0, 0);
+    if (nsub > 1) read_kfrag<D>(ring + AC::kSlotBytes, kf);
+  }
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // as at every barrier: no LDS read in flight into the loop
+  int cur = 0;  // slot of sub-tile t
   for (int t = 0; t < nsub; ++t) {
-    const int cur = t & 1, nxt = cur ^ 1;
-    uint4 vn = make_uint4(0, 0, 0, 0);
-    if (t + 1 < nsub) {
-      stage_k<D>((const char*)ksrc, 32 * (t + 1), u.ntok, kst[nxt], wave);
-      vn = load_v<D>(vsrc, 32 * (t + 1), u.ntok);
+    const char* slot = ring + cur * AC::kSlotBytes;
+    const int nxt = cur + 1 == RING ? 0 : cur + 1;
+    if (t + RING - 1 < nsub) {
+      const int fill = cur == 0 ? RING - 1 : cur - 1;  // the slot of sub-tile t - 1, read before the last barrier
+      copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(fill * AC::kSlotBytes), wave);
     }
     if (active) {
-      Frag kf[KS];
-      read_kfrag<D>(kst[cur], kf);
-      f32x16 acc = {};
+      // sc[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
+      if (32 * (t + 1) > ntok || u.guide) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, acc, 0, 0, 0);
-      // acc[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
-      float mx = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int tok = 32 * t + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-        const bool seen = tok < u.ntok && (!u.guide || tok <= j);
-        acc[i] = seen ? acc[i] : -INFINITY;
-        mx = fmaxf(mx, acc[i]);
+        for (int i = 0; i < 16; ++i) {
+          const int tok = 32 * t + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+          const bool seen = tok < ntok && (!u.guide || tok <= jrow);
+          sc[i] = seen ? sc[i] : -INFINITY;
+        }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * a.c;  // the row's maximum over the sub-tile (c > 0)
-      const bool raise = mx > m + kLazyRaise;
-      if (__builtin_amdgcn_ballot_w64(raise)) {  // rare after a row's first sub-tile
-        const float mn = raise ? mx : m;
-        const float al = __builtin_amdgcn_exp2f(m - mn);
-        lsum *= al;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) ot[db][i] *= al;
-        m = mn;
-      }
+      // S of sub-tile t + 1 (past the end: a repeat of the last sub-tile, never used) and
+      // O += V P of sub-tile t - 1, one MFMA of each per step (S first: its chain is
+      // dependent), each step also computing 16 / KS of the exponentials of sub-tile t; the
+      // scheduling barriers keep the steps in this order.
+      static_assert(KS == 2 * NDB, "as many S steps as O steps");
+      constexpr int TPS = 16 / KS;  // terms per step
+      f32x16 sn = {};
       float p[16];
-      float ps = 0.f;
+      float e[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        p[i] = __builtin_amdgcn_exp2f(fmaf(acc[i], a.c, -m));
-        ps += p[i];
+      for (int s = 0; s < KS; ++s) {
+        sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, sn, 0, 0, 0);
+        ot[s % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[s % NDB][s / NDB].v, pb[s / NDB], ot[s % NDB], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < TPS; ++j) {
+          const int i = TPS * s + j;
+          p[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], a.c, -m));
+          e[i & 3] += p[i];
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x400, TPS, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      float ps = (e[0] + e[1]) + (e[2] + e[3]);
+      const bool big = !(ps < kAttnLazyLimit);
+      const uint64_t bal = __builtin_amdgcn_ballot_w64(big);
+      if (bal) {
+        const uint32_t pair = (uint32_t)bal | (uint32_t)(bal >> 32);
+        if ((pair >> (lane & 31)) & 1u) raise_max<NDB>(sc, a.c, m, lsum, ot, p, ps);
       }
       lsum += ps;
-      bf16x8 pb[2];
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
+      // the next iteration's operands (landed at the last barrier): V of sub-tile t, the K
+      // fragments of sub-tile t + 2
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const Frag vf = read_vfrag(vts[cur], db, s2);
-          ot[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pb[s2], ot[db], 0, 0, 0);
-        }
+        for (int s2 = 0; s2 < 2; ++s2) vf[db][s2] = read_vfrag<D>(slot + AC::kTileBytes, db, s2);
+      if (t + 2 < nsub) {
+        const int s2slot = nxt + 1 == RING ? 0 : nxt + 1;
+        read_kfrag<D>(ring + s2slot * AC::kSlotBytes, kf);
+      }
+      sc = sn;
     }
-    if (t + 1 < nsub) write_vt<D>(vts[nxt], vn);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    // sub-tile t + 3 has landed for every wave; copies of t + 4 .. may stay in flight
+    wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 3), 0));
+    ring_barrier();
+    cur = nxt;
+  }
+  if (active) {  // O += V P of the last sub-tile
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+        ot[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db][s2].v, pb[s2], ot[db], 0, 0, 0);
   }
   if (!active) return;
   lsum += __shfl_xor(lsum, 32);  // the row's other 16 tokens of every sub-tile
