@@ -50,24 +50,38 @@ tp_status check_dims(const tp_dims* d) {
 tp_status check_offsets(const int64_t* off, int32_t batch, const char* what, bool allow_empty_seq) {
   if (!off) return fail(TP_ERR_NULL, "%s is NULL", what);
   if (off[0] != 0) return fail(TP_ERR_SHAPE, "%s[0] must be 0", what);
-  for (int b = 0; b < batch; ++b) {
-    const int64_t n = off[b + 1] - off[b];
-    if (n < (allow_empty_seq ? 0 : 1))
-      return fail(TP_ERR_SHAPE, "%s: entry %d has length %lld", what, b, (long long)n);
-  }
+  for (int b = 0; b < batch; ++b)  // compared, not subtracted: arbitrary entries cannot overflow
+    if (off[b + 1] < off[b] || (!allow_empty_seq && off[b + 1] == off[b]))
+      return fail(TP_ERR_SHAPE, "%s: entry %d is empty or negative (%lld -> %lld)", what, b, (long long)off[b],
+                  (long long)off[b + 1]);
   return TP_OK;
 }
 
-tp_status check_batch(const tp_batch* bt, bool need_guides) {
+// The batch's offsets (nondecreasing from 0, each sequence non-empty), and extents for which
+// every size the layouts, tables and launches derive from them fits in 64 bits: at most 2^40
+// context tokens and 2^52 token-heads, 2^31 - 1 guide tokens and 2^40 guide rows, and at most
+// 2^60 bytes of per-chunk row partials (chunks of 8192 tokens, the smallest any kernel uses).
+// The bounds are far above any cache a GPU holds.  `d` has passed check_dims.
+tp_status check_batch(const tp_dims* d, const tp_batch* bt, bool need_guides) {
   if (!bt) return fail(TP_ERR_NULL, "batch is NULL");
   if (bt->batch < 1) return fail(TP_ERR_SHAPE, "batch must be >= 1");
   if (bt->batch > TP_MAX_BATCH)
     return fail(TP_ERR_UNSUPPORTED, "batch %d exceeds TP_MAX_BATCH (%d)", bt->batch, TP_MAX_BATCH);
   tp_status s = check_offsets(bt->ctx_offsets, bt->batch, "ctx_offsets", false);
   if (s != TP_OK) return s;
+  const double n_tot = (double)bt->ctx_offsets[bt->batch];
+  if (n_tot > 0x1p40 || n_tot * d->num_layers * d->num_kv_heads > 0x1p52)
+    return fail(TP_ERR_UNSUPPORTED, "context of %lld tokens too large", (long long)bt->ctx_offsets[bt->batch]);
   if (need_guides) {
     s = check_offsets(bt->guide_offsets, bt->batch, "guide_offsets", false);
     if (s != TP_OK) return s;
+    int64_t max_nb = 0;
+    for (int b = 0; b < bt->batch; ++b) max_nb = std::max<int64_t>(max_nb, bt->ctx_offsets[b + 1] - bt->ctx_offsets[b]);
+    const double g_tot = (double)bt->guide_offsets[bt->batch];
+    const double rows = g_tot * d->num_layers * d->num_q_heads;
+    if (g_tot > 0x1p31 - 1 || rows > 0x1p40 || rows * ((double)max_nb / 8192.0 + 2.0) * (8.0 + 4.0 * d->head_dim) > 0x1p60)
+      return fail(TP_ERR_UNSUPPORTED, "guide of %lld tokens too large for this context",
+                  (long long)bt->guide_offsets[bt->batch]);
   }
   return TP_OK;
 }
@@ -117,7 +131,7 @@ tp_status prepare_guide(const tp_dims* dims, const tp_batch* batch, const void* 
                         float* s_key, void* workspace, size_t ws_bytes, tp::GuideArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, true);
+  s = check_batch(dims, batch, true);
   if (s != TP_OK) return s;
   if (!q_guide || !k || !s_key) return fail(TP_ERR_NULL, "q_guide, k and s_key must be non-NULL");
   if (!aligned16(q_guide) || !aligned16(k) || !aligned16(s_key) || (k_guide && !aligned16(k_guide)))
@@ -181,7 +195,7 @@ tp_status prepare_quant(const tp_dims* dims, const tp_batch* batch, const void* 
                         float* scales, void* v_q, tp::QuantArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, false);
+  s = check_batch(dims, batch, false);
   if (s != TP_OK) return s;
   s = check_qfmt(qfmt, bits);
   if (s != TP_OK) return s;
@@ -204,7 +218,7 @@ tp_status prepare_select(const tp_dims* dims, const tp_batch* batch, const float
                          int32_t* kept_idx, float* s_out, void* workspace, size_t ws_bytes, tp::SelectArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, false);
+  s = check_batch(dims, batch, false);
   if (s != TP_OK) return s;
   if (!s_key || !scales || !kept_idx) return fail(TP_ERR_NULL, "s_key, scales and kept_idx must be non-NULL");
   if (!aligned16(s_key) || !aligned16(scales) || !aligned16(kept_idx) || (s_out && !aligned16(s_out)))
@@ -220,7 +234,7 @@ tp_status prepare_select(const tp_dims* dims, const tp_batch* batch, const float
   for (int b = 0; b < batch->batch; ++b) {
     const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
     const int64_t kb = tp_keep_count(nb, keep_ratio, keep_budget);
-    if (kept_offsets[b + 1] - kept_offsets[b] != kb)
+    if (kept_offsets[b + 1] < kept_offsets[b] || kept_offsets[b + 1] - kept_offsets[b] != kb)
       return fail(TP_ERR_SHAPE, "kept_offsets[%d+1]-kept_offsets[%d] = %lld, expected keep count %lld", b, b,
                   (long long)(kept_offsets[b + 1] - kept_offsets[b]), (long long)kb);
     a.k[b] = kb;
@@ -274,7 +288,7 @@ tp_status prepare_compact(const tp_dims* dims, const tp_batch* batch, const int6
                           tp::CompactArgs& a) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, false);
+  s = check_batch(dims, batch, false);
   if (s != TP_OK) return s;
   s = check_qfmt(qfmt, bits);
   if (s != TP_OK) return s;
@@ -290,8 +304,10 @@ tp_status prepare_compact(const tp_dims* dims, const tp_batch* batch, const int6
   memset(&a, 0, sizeof a);
   for (int b = 0; b < batch->batch; ++b) {
     const int64_t nb = batch->ctx_offsets[b + 1] - batch->ctx_offsets[b];
+    if (kept_offsets[b + 1] < kept_offsets[b])  // entries from 0 up: their differences cannot overflow
+      return fail(TP_ERR_SHAPE, "kept_offsets decrease at entry %d", b);
     const int64_t kb = kept_offsets[b + 1] - kept_offsets[b];
-    if (kb < 0 || kb > nb)
+    if (kb > nb)
       return fail(TP_ERR_SHAPE, "kept count of sequence %d (%lld) outside [0, %lld]", b, (long long)kb, (long long)nb);
     a.kept_off[b] = kept_offsets[b];
   }
@@ -436,7 +452,11 @@ int64_t tp_keep_count(int64_t n, double keep_ratio, int64_t keep_budget) {
   if (use_ratio == use_budget) return -1;
   if (use_ratio) {
     if (!(keep_ratio <= 1.0)) return -1;
-    const int64_t k = (int64_t)floor((double)n * keep_ratio);
+    // k <= n; (double)n can round above n (to 2^63 at the top of the range), so compare
+    // before converting back
+    const double kd = floor((double)n * keep_ratio);
+    if (kd >= (double)n) return n;
+    const int64_t k = (int64_t)kd;
     return k < 1 ? 1 : k;
   }
   return keep_budget < n ? keep_budget : n;
@@ -447,7 +467,7 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
   if (fn == TP_FN_GUIDE_SCORES) {
-    s = check_batch(batch, true);
+    s = check_batch(dims, batch, true);
     if (s != TP_OK) return s;
     *bytes = tp::guide_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads,
                                         batch->ctx_offsets, batch->guide_offsets, batch->batch)
@@ -455,13 +475,13 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
     return ok();
   }
   if (fn == TP_FN_COMBINE_SELECT_TOPK) {
-    s = check_batch(batch, false);
+    s = check_batch(dims, batch, false);
     if (s != TP_OK) return s;
     *bytes = select_workspace(dims, batch);
     return ok();
   }
   if (fn == TP_FN_GUIDE_ATTENTION) {
-    s = check_batch(batch, true);
+    s = check_batch(dims, batch, true);
     if (s != TP_OK) return s;
     *bytes = tp::attn_workspace_layout(dims->num_layers, dims->num_q_heads, dims->num_kv_heads, dims->head_dim,
                                        batch->ctx_offsets, batch->guide_offsets, batch->batch)
@@ -469,7 +489,7 @@ tp_status tp_workspace_size(int32_t fn, const tp_dims* dims, const tp_batch* bat
     return ok();
   }
   if (fn == TP_FN_EVICT) {
-    s = check_batch(batch, true);
+    s = check_batch(dims, batch, true);
     if (s != TP_OK) return s;
     *bytes = evict_workspace_bytes(dims, batch);
     return ok();
@@ -507,7 +527,7 @@ tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const v
                              float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, true);
+  s = check_batch(dims, batch, true);
   if (s != TP_OK) return s;
   if (!q_guide || !k || !v || !o_guide || !guide_lse)
     return fail(TP_ERR_NULL, "q_guide, k, v, o_guide and guide_lse must be non-NULL");
@@ -645,7 +665,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   }
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
-  s = check_batch(batch, true);
+  s = check_batch(dims, batch, true);
   if (s != TP_OK) return s;
   // workspace: the score pass's, then (without s_out) the combined scores
   const size_t gws = guide_workspace_bytes(dims, batch);
