@@ -53,39 +53,73 @@ def _run_attention(w, guide_keys):
         lse.cpu().numpy().reshape(w.L, w.Hq, w.g_tot)
 
 
+def _check_rows(w, b, l, h, qheads, o_gpu, lse_gpu, guide_keys):
+    """The oracle's output and normaliser for the guide rows of query heads `qheads` (of KV
+    head h) of sequence b, layer l, against the GPU's; returns the worst output error (as a
+    fraction of the weighted |v|) and the worst normaliser error."""
+    g = w.guide_lens[b]
+    goff = w.guide_offsets()
+    _, kb, vb = pu.host_segment(w, b, l, h)
+    kr, vr = o.bf16_to_f64(kb), o.bf16_to_f64(vb)
+    kg = o.bf16_to_f64(pu.host_guide_keys(w, b, l, h)) if guide_keys else None
+    vg = o.bf16_to_f64(pu.host_guide_values(w, b, l, h)) if guide_keys else None
+    worst_o = worst_l = 0.0
+    for qh in qheads:
+        qr = o.bf16_to_f64(synth.rows(w.q, b, l, qh, g, w.d))
+        ref = o.guide_attention_output(qr, kr, vr, w.softmax_scale, kg, vg)
+        mag = o.guide_attention_output(qr, kr, np.abs(vr), w.softmax_scale, kg, None if vg is None else np.abs(vg))
+        got = o_gpu[l, qh, goff[b]:goff[b] + g].astype(np.float64)
+        err = np.abs(got - ref)
+        tag = f"{w.name} b={b} l={l} qh={qh}"
+        assert np.all(np.isfinite(got)), tag
+        assert np.all(err <= 2.0 ** -8 * mag + 1e-7), (tag, float((err / (mag + 1e-30)).max()))
+        worst_o = max(worst_o, float((err / (mag + 1e-30)).max()))
+        lref = o.guide_log_normalisers(qr, kr, w.softmax_scale, kg)
+        lgot = lse_gpu[l, qh, goff[b]:goff[b] + g].astype(np.float64)
+        assert np.all(np.abs(lgot - lref) <= 1e-4), (tag, float(np.abs(lgot - lref).max()))
+        worst_l = max(worst_l, float(np.abs(lgot - lref).max()))
+    return worst_o, worst_l
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_guide_attention_parity(gpu_lib, case):
     w = _workload(case)
     guide_keys = case[-1]
     pu.log(f"guide attention {w.name}: {w.describe()}, guide keys {guide_keys}")
     _, o_gpu, lse_gpu = _run_attention(w, guide_keys)
-    goff = w.guide_offsets()
     worst_o = worst_l = 0.0
     for b in range(w.batch):
-        g = w.guide_lens[b]
         for l in range(w.L):
             for h in range(w.Hkv):
-                _, kb, vb = pu.host_segment(w, b, l, h)
-                kr, vr = o.bf16_to_f64(kb), o.bf16_to_f64(vb)
-                kg = o.bf16_to_f64(pu.host_guide_keys(w, b, l, h)) if guide_keys else None
-                vg = o.bf16_to_f64(pu.host_guide_values(w, b, l, h)) if guide_keys else None
-                for r in range(w.R):
-                    qh = h * w.R + r
-                    qr = o.bf16_to_f64(synth.rows(w.q, b, l, qh, g, w.d))
-                    ref = o.guide_attention_output(qr, kr, vr, w.softmax_scale, kg, vg)
-                    mag = o.guide_attention_output(qr, kr, np.abs(vr), w.softmax_scale, kg,
-                                                   None if vg is None else np.abs(vg))
-                    got = o_gpu[l, qh, goff[b]:goff[b] + g].astype(np.float64)
-                    err = np.abs(got - ref)
-                    tag = f"{w.name} b={b} l={l} qh={qh}"
-                    assert np.all(np.isfinite(got)), tag
-                    assert np.all(err <= 2.0 ** -8 * mag + 1e-7), (tag, float((err / (mag + 1e-30)).max()))
-                    worst_o = max(worst_o, float((err / (mag + 1e-30)).max()))
-                    lref = o.guide_log_normalisers(qr, kr, w.softmax_scale, kg)
-                    lgot = lse_gpu[l, qh, goff[b]:goff[b] + g].astype(np.float64)
-                    assert np.all(np.abs(lgot - lref) <= 1e-4), (tag, float(np.abs(lgot - lref).max()))
-                    worst_l = max(worst_l, float(np.abs(lgot - lref).max()))
+                wo, wl = _check_rows(w, b, l, h, range(h * w.R, (h + 1) * w.R), o_gpu, lse_gpu, guide_keys)
+                worst_o, worst_l = max(worst_o, wo), max(worst_l, wl)
     pu.log(f"  output error <= {worst_o:.3g} of the weighted |v|, normaliser error <= {worst_l:.3g}")
+
+
+# The full-size workloads in the launch configuration `bench.py --prefill-attention` times,
+# guide keys included (contexts of 131072 tokens or more take 32768-token chunks, shorter ones
+# 8192): every output and normaliser finite, and sampled (sequence, layer, KV head, query
+# head) rows against the oracle.
+FULL = {
+    "llama8b_128k": [(0, 0, 0, 0), (0, 17, 3, 14), (0, 31, 7, 31)],
+    "llama8b_32k": [(0, 16, 3, 13)],
+    "ragged8": [(2, 9, 2, 9), (7, 31, 7, 30)],
+}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_guide_attention_fullsize_sampled(gpu_lib, name):
+    w = W.ALL[name]()
+    pu.log(f"guide attention, full size: {w.describe()}")
+    torch.cuda.empty_cache()
+    tensors, o_gpu, lse_gpu = _run_attention(w, True)
+    del tensors
+    torch.cuda.empty_cache()
+    assert np.all(np.isfinite(o_gpu)) and np.all(np.isfinite(lse_gpu))
+    for (b, l, h, qh) in FULL[name]:
+        assert qh // w.R == h
+        wo, wl = _check_rows(w, b, l, h, [qh], o_gpu, lse_gpu, True)
+        pu.log(f"  b={b} l={l} qh={qh}: output error <= {wo:.3g} of the weighted |v|, normaliser error <= {wl:.3g}")
 
 
 @pytest.mark.parametrize("case", [CASES[2], CASES[4]], ids=[CASES[2][0], CASES[4][0]])
