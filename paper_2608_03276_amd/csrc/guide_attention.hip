@@ -142,13 +142,6 @@ __device__ inline Frag read_vfrag(const char* vtile, int db, int s2) {
   return f;
 }
 
-__device__ inline float max16(const f32x16& x) {
-  const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
-  const float a2 = fmaxf(fmaxf(x[6], x[7]), x[8]), a3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
-  const float a4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
-  return fmaxf(fmaxf(fmaxf(a0, a1), x[15]), fmaxf(fmaxf(a2, a3), a4));
-}
-
 __device__ inline float terms(const f32x16& s, float c, float m, float (&p)[16]) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(fmaf(s[i], c, -m));

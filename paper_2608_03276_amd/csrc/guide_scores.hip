@@ -188,13 +188,6 @@ __device__ inline void step_schedule() {
 // compiler sinks it past the loop's branches, away from the MFMAs it should overlap.
 __device__ inline void pin(float a, float b, float c, float d) { asm volatile("" ::"v"(a), "v"(b), "v"(c), "v"(d)); }
 
-__device__ inline float max16(const f32x16& x) {
-  const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
-  const float a2 = fmaxf(fmaxf(x[6], x[7]), x[8]), a3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
-  const float a4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
-  return fmaxf(fmaxf(fmaxf(a0, a1), x[15]), fmaxf(fmaxf(a2, a3), a4));
-}
-
 // ---------------------------------------------------------------------------- pass 1
 // Online (max, sum) of one unit (32 tokens x 32 rows): acc[i] is the logit of token
 // (i/4)*8 + (lane/32)*4 + i%4 and row lane%32.  c > 0, so max(x) * c = max(x * c).

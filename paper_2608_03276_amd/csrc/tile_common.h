@@ -53,6 +53,14 @@ __device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) 
   }
 }
 
+// The largest of the 16 accumulator values a lane holds.
+__device__ inline float max16(const f32x16& x) {
+  const float a0 = fmaxf(fmaxf(x[0], x[1]), x[2]), a1 = fmaxf(fmaxf(x[3], x[4]), x[5]);
+  const float a2 = fmaxf(fmaxf(x[6], x[7]), x[8]), a3 = fmaxf(fmaxf(x[9], x[10]), x[11]);
+  const float a4 = fmaxf(fmaxf(x[12], x[13]), x[14]);
+  return fmaxf(fmaxf(fmaxf(a0, a1), x[15]), fmaxf(fmaxf(a2, a3), a4));
+}
+
 // Running (max, sum) statistics start at (-FLT_MAX, 0) rather than (-inf, 0): merging a
 // unit whose logits are all -inf (masked tokens, or the empty pipeline slot before the
 // first pair) is then an exact no-op, with no special case.
