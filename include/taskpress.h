@@ -93,6 +93,8 @@ typedef struct tp_batch {
   const int64_t* guide_offsets; /* host [B+1]: guide tokens of sequence b, G_b >= 1 (for
                                    tp_guide_scores; may be NULL for the other calls) */
 } tp_batch;
+/* Size limits (TP_ERR_UNSUPPORTED beyond them; far above what one GPU holds): N_tot <= 2^30;
+ * with guides G_tot <= 2^31 - 1, L * Hq * G_tot <= 2^32 and L * Hq * G_b <= 2^26 for every b. */
 
 /* Version string of the library. */
 const char* tp_version(void);

@@ -58,10 +58,13 @@ tp_status check_offsets(const int64_t* off, int32_t batch, const char* what, boo
 }
 
 // The batch's offsets (nondecreasing from 0, each sequence non-empty), and extents for which
-// every size the layouts, tables and launches derive from them fits in 64 bits: at most 2^40
-// context tokens and 2^52 token-heads, 2^31 - 1 guide tokens and 2^40 guide rows, and at most
-// 2^60 bytes of per-chunk row partials (chunks of 8192 tokens, the smallest any kernel uses).
-// The bounds are far above any cache a GPU holds.  `d` has passed check_dims.
+// every size the layouts derive fits in 64 bits and every launch fits its grid (a dispatch
+// holds fewer than 2^32 work-items per dimension): at most 2^30 context tokens per (layer,
+// head) (the gather launches 4 work-items per kept token; kept indices are int32), at most
+// 2^32 guide rows in all and 2^26 per sequence (the row merges launch a work-item per row and
+// 64 per row), 2^31 - 1 guide tokens, and 2^60 bytes of per-chunk row partials (chunks of
+// 8192 tokens, the smallest any kernel uses).  Far above any cache one GPU holds.  `d` has
+// passed check_dims.
 tp_status check_batch(const tp_dims* d, const tp_batch* bt, bool need_guides) {
   if (!bt) return fail(TP_ERR_NULL, "batch is NULL");
   if (bt->batch < 1) return fail(TP_ERR_SHAPE, "batch must be >= 1");
@@ -69,18 +72,23 @@ tp_status check_batch(const tp_dims* d, const tp_batch* bt, bool need_guides) {
     return fail(TP_ERR_UNSUPPORTED, "batch %d exceeds TP_MAX_BATCH (%d)", bt->batch, TP_MAX_BATCH);
   tp_status s = check_offsets(bt->ctx_offsets, bt->batch, "ctx_offsets", false);
   if (s != TP_OK) return s;
-  const double n_tot = (double)bt->ctx_offsets[bt->batch];
-  if (n_tot > 0x1p40 || n_tot * d->num_layers * d->num_kv_heads > 0x1p52)
-    return fail(TP_ERR_UNSUPPORTED, "context of %lld tokens too large", (long long)bt->ctx_offsets[bt->batch]);
+  if (bt->ctx_offsets[bt->batch] > ((int64_t)1 << 30))
+    return fail(TP_ERR_UNSUPPORTED, "context of %lld tokens too large (at most 2^30)",
+                (long long)bt->ctx_offsets[bt->batch]);
   if (need_guides) {
     s = check_offsets(bt->guide_offsets, bt->batch, "guide_offsets", false);
     if (s != TP_OK) return s;
-    int64_t max_nb = 0;
-    for (int b = 0; b < bt->batch; ++b) max_nb = std::max<int64_t>(max_nb, bt->ctx_offsets[b + 1] - bt->ctx_offsets[b]);
+    int64_t max_nb = 0, max_gb = 0;
+    for (int b = 0; b < bt->batch; ++b) {
+      max_nb = std::max<int64_t>(max_nb, bt->ctx_offsets[b + 1] - bt->ctx_offsets[b]);
+      max_gb = std::max<int64_t>(max_gb, bt->guide_offsets[b + 1] - bt->guide_offsets[b]);
+    }
     const double g_tot = (double)bt->guide_offsets[bt->batch];
-    const double rows = g_tot * d->num_layers * d->num_q_heads;
-    if (g_tot > 0x1p31 - 1 || rows > 0x1p40 || rows * ((double)max_nb / 8192.0 + 2.0) * (8.0 + 4.0 * d->head_dim) > 0x1p60)
-      return fail(TP_ERR_UNSUPPORTED, "guide of %lld tokens too large for this context",
+    const double heads = (double)d->num_layers * d->num_q_heads;
+    const double rows = g_tot * heads;
+    if (g_tot > 0x1p31 - 1 || rows > 0x1p32 || (double)max_gb * heads > 0x1p26 ||
+        rows * ((double)max_nb / 8192.0 + 2.0) * (8.0 + 4.0 * d->head_dim) > 0x1p60)
+      return fail(TP_ERR_UNSUPPORTED, "guide of %lld tokens too large for these dims and context",
                   (long long)bt->guide_offsets[bt->batch]);
   }
   return TP_OK;

@@ -2,9 +2,8 @@
 // entry point with arguments that must fail validation, the host-only helpers at their edges,
 // offsets and shapes chosen to overflow careless size arithmetic, and, only when the HIP
 // runtime sees no device, well-formed calls that must end in TP_ERR_HIP.  The library under
-// test is built for the host only (no device code), with AddressSanitizer and UBSan; fake
-// device pointers are never dereferenced by correct host code.  Exit status 0 when every
-// check holds.
+// test is built with AddressSanitizer and UBSan on its host side; fake device pointers are
+// never dereferenced by correct host code.  Exit status 0 when every check holds.
 #include <hip/hip_runtime_api.h>
 
 #include <climits>
@@ -178,6 +177,17 @@ void hostile_shapes() {
     EXPECT_TRUE(s == TP_ERR_UNSUPPORTED || s == TP_ERR_SHAPE);
     const tp_status s2 = tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, &big, &bt.c, &n);
     EXPECT_TRUE(s2 == TP_ERR_UNSUPPORTED || s2 == TP_ERR_SHAPE);
+  }
+  {
+    // past the launch limits though the sizes fit in 64 bits: 2^30 + 1 context tokens, and
+    // 2^26 + 1 guide rows of one sequence
+    Batch wide({0, ((int64_t)1 << 30) + 1}, {0, 16});
+    EXPECT(tp_workspace_size(TP_FN_COMBINE_SELECT_TOPK, &d, &wide.c, &n), TP_ERR_UNSUPPORTED);
+    const tp_dims one{1, 1, 1, 64};
+    Batch rows({0, 100}, {0, ((int64_t)1 << 26) + 1});
+    EXPECT(tp_workspace_size(TP_FN_GUIDE_ATTENTION, &one, &rows.c, &n), TP_ERR_UNSUPPORTED);
+    Batch rows_ok({0, 100}, {0, (int64_t)1 << 20});
+    EXPECT(tp_workspace_size(TP_FN_GUIDE_ATTENTION, &one, &rows_ok.c, &n), TP_OK);
   }
   {
     const tp_dims neg{-2, 8, 2, 64};
