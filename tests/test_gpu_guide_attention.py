@@ -28,6 +28,10 @@ CASES = [
     ("chunk-edges", 1, 8, 2, 128, [8192, 16384, 16385], [64, 9, 40], True),
     ("two-row-groups", 1, 16, 2, 128, [3000, 700], [40, 33], True),
     ("outliers-no-guide-keys", 1, 8, 2, 128, [4500], [64], False),
+    # degenerate: one query head per KV head, single guide tokens, a one-token context
+    ("mha-one-row", 2, 2, 2, 64, [1, 5000, 33], [1, 1, 2], True),
+    # head dim 64 with guide keys over the 8192-token chunk edge and a long guide
+    ("d64-chunk-edge", 1, 8, 2, 64, [8193, 40], [200, 1], True),
 ]
 
 
