@@ -41,7 +41,8 @@ struct AttnCfg {
   static constexpr int kCopies = kSlotBytes / 1024 / kAttnWaves;  // 1 KB copies per wave per sub-tile
   static constexpr int kRing = D == 128 ? 9 : 16;             // slots: 144 KB / 128 KB of LDS
   static_assert(kRing * kSlotBytes <= 160 * 1024, "LDS of one CU");
-  static_assert(kRing - 4 <= 12 && (kRing - 4) * kCopies <= 63, "wait_copies_but cases and the vmcnt range");
+  static_assert(kRing >= 7 && kRing - 6 <= 12 && (kRing - 6) * kCopies <= 63,
+                "the pair protocol's lookahead, wait_copies_but cases and the vmcnt range");
 };
 
 // V sub-tiles are staged like K (16-byte piece p of token tl in slot p ^ swzv(tl)) with their
@@ -84,7 +85,7 @@ __device__ inline void copy_subtile(const char* kbase, const char* vbase, int t0
 }
 
 // Wait until at most k sub-tiles' copies of this wave are still in flight (copies complete in
-// issue order).  k is wave-uniform and at most kRing - 4 (12).
+// issue order).  k is wave-uniform and at most kRing - 6 (12).
 template <int PER>
 __device__ inline void wait_copies_but(int k) {
   switch (k) {
@@ -263,13 +264,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   // those exponentials, so the matrix pipe has work while the vector ALU computes them); then
   // it reads the V fragments of sub-tile t and the K fragments of sub-tile t + 2, so every
   // operand of the next iteration is in registers when it starts.  A raise of the maximum in
-  // iteration t rescales O after sub-tile t - 1 has been added with the old maximum.  The
-  // copies run RING - 1 sub-tiles ahead; the barrier closing iteration t follows the landing
-  // of sub-tile t + 3.
-  // prologue: sub-tiles 0 .. RING-2 in flight; 0, 1 and 2 landed before the loop
-  for (int t = 0; t < RING - 1 && t < nsub; ++t)
+  // iteration t rescales O after sub-tile t - 1 has been added with the old maximum.
+  // Sub-tile x lives in ring slot x mod RING; its last reads are those of iteration x.  The
+  // iterations run in pairs (t even, t + 1) with one barrier after each pair: after it, the
+  // copies of sub-tiles t + RING - 2 and t + RING - 1 go into the slots of t - 2 and t - 1,
+  // and the barrier closing iteration t + 1 follows the landing of sub-tile t + 5 (the last
+  // one the next pair reads).
+  // prologue: sub-tiles 0 .. RING-3 in flight; 0 .. 3 landed before the loop
+  for (int t = 0; t < RING - 2 && t < nsub; ++t)
     copy_subtile<D>(kb, vb, 32 * t, ntok, ring_lds + (uint32_t)(t * AC::kSlotBytes), wave);
-  wait_copies_but<AC::kCopies>(max(min(RING - 2, nsub - 1) - 2, 0));
+  wait_copies_but<AC::kCopies>(max(min(RING - 3, nsub - 1) - 3, 0));
   ring_barrier();
   Frag kf[KS];
   Frag vf[NDB][2];  // V of the sub-tile whose O += V P is pending (zero before the first)
@@ -285,76 +289,84 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     if (nsub > 1) read_kfrag<D>(ring + AC::kSlotBytes, kf);
   }
   __builtin_amdgcn_s_waitcnt(0xC07F);  // as at every barrier: no LDS read in flight into the loop
-  int cur = 0;  // slot of sub-tile t
-  for (int t = 0; t < nsub; ++t) {
+  // iteration t of the pipeline, with `cur` the slot of sub-tile t
+  const auto iteration = [&](int t, int cur) {
     const char* slot = ring + cur * AC::kSlotBytes;
-    const int nxt = cur + 1 == RING ? 0 : cur + 1;
-    if (t + RING - 1 < nsub) {
-      const int fill = cur == 0 ? RING - 1 : cur - 1;  // the slot of sub-tile t - 1, read before the last barrier
-      copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(fill * AC::kSlotBytes), wave);
+    // sc[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
+    if (32 * (t + 1) > ntok || u.guide) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int tok = 32 * t + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+        const bool seen = tok < ntok && (!u.guide || tok <= jrow);
+        sc[i] = seen ? sc[i] : -INFINITY;
+      }
     }
+    // S of sub-tile t + 1 (past the end: a repeat of the last sub-tile, never used) and
+    // O += V P of sub-tile t - 1, one MFMA of each per step (S first: its chain is
+    // dependent), each step also computing 16 / KS of the exponentials of sub-tile t; the
+    // scheduling barriers keep the steps in this order.
+    static_assert(KS == 2 * NDB, "as many S steps as O steps");
+    constexpr int TPS = 16 / KS;  // terms per step
+    f32x16 sn = {};
+    float p[16];
+    float e[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, sn, 0, 0, 0);
+      ot[s % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[s % NDB][s / NDB].v, pb[s / NDB], ot[s % NDB], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < TPS; ++j) {
+        const int i = TPS * s + j;
+        p[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], a.c, -m));
+        e[i & 3] += p[i];
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x400, TPS, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float ps = (e[0] + e[1]) + (e[2] + e[3]);
+    const bool big = !(ps < kAttnLazyLimit);
+    const uint64_t bal = __builtin_amdgcn_ballot_w64(big);
+    if (bal) {
+      const uint32_t pair = (uint32_t)bal | (uint32_t)(bal >> 32);
+      if ((pair >> (lane & 31)) & 1u) raise_max<NDB>(sc, a.c, m, lsum, ot, p, ps);
+    }
+    lsum += ps;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
+    // the next iteration's operands (landed at the last barrier): V of sub-tile t, the K
+    // fragments of sub-tile t + 2
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) vf[db][s2] = read_vfrag<D>(slot + AC::kTileBytes, db, s2);
+    if (t + 2 < nsub) {
+      const int k2 = cur + 2 >= RING ? cur + 2 - RING : cur + 2;
+      read_kfrag<D>(ring + k2 * AC::kSlotBytes, kf);
+    }
+    sc = sn;
+  };
+  int cur = 0;  // slot of sub-tile t
+  for (int t = 0; t < nsub; t += 2) {
+    // the slots of sub-tiles t - 2 and t - 1, read before the last barrier
+    const int f1 = cur >= 2 ? cur - 2 : cur + RING - 2;
+    const int f2 = cur >= 1 ? cur - 1 : cur + RING - 1;
+    if (t + RING - 2 < nsub)
+      copy_subtile<D>(kb, vb, 32 * (t + RING - 2), ntok, ring_lds + (uint32_t)(f1 * AC::kSlotBytes), wave);
+    if (t + RING - 1 < nsub)
+      copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
+    const int c1 = cur + 1 == RING ? 0 : cur + 1;
     if (active) {
-      // sc[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
-      if (32 * (t + 1) > ntok || u.guide) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int tok = 32 * t + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-          const bool seen = tok < ntok && (!u.guide || tok <= jrow);
-          sc[i] = seen ? sc[i] : -INFINITY;
-        }
-      }
-      // S of sub-tile t + 1 (past the end: a repeat of the last sub-tile, never used) and
-      // O += V P of sub-tile t - 1, one MFMA of each per step (S first: its chain is
-      // dependent), each step also computing 16 / KS of the exponentials of sub-tile t; the
-      // scheduling barriers keep the steps in this order.
-      static_assert(KS == 2 * NDB, "as many S steps as O steps");
-      constexpr int TPS = 16 / KS;  // terms per step
-      f32x16 sn = {};
-      float p[16];
-      float e[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, sn, 0, 0, 0);
-        ot[s % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[s % NDB][s / NDB].v, pb[s / NDB], ot[s % NDB], 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < TPS; ++j) {
-          const int i = TPS * s + j;
-          p[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], a.c, -m));
-          e[i & 3] += p[i];
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x400, TPS, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      float ps = (e[0] + e[1]) + (e[2] + e[3]);
-      const bool big = !(ps < kAttnLazyLimit);
-      const uint64_t bal = __builtin_amdgcn_ballot_w64(big);
-      if (bal) {
-        const uint32_t pair = (uint32_t)bal | (uint32_t)(bal >> 32);
-        if ((pair >> (lane & 31)) & 1u) raise_max<NDB>(sc, a.c, m, lsum, ot, p, ps);
-      }
-      lsum += ps;
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
-      // the next iteration's operands (landed at the last barrier): V of sub-tile t, the K
-      // fragments of sub-tile t + 2
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) vf[db][s2] = read_vfrag<D>(slot + AC::kTileBytes, db, s2);
-      if (t + 2 < nsub) {
-        const int s2slot = nxt + 1 == RING ? 0 : nxt + 1;
-        read_kfrag<D>(ring + s2slot * AC::kSlotBytes, kf);
-      }
-      sc = sn;
+      iteration(t, cur);
+      if (t + 1 < nsub) iteration(t + 1, c1);
     }
-    // sub-tile t + 3 has landed for every wave; copies of t + 4 .. may stay in flight
-    wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 3), 0));
+    // sub-tile t + 5 has landed for every wave; copies of t + 6 .. may stay in flight
+    wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 5), 0));
     ring_barrier();
-    cur = nxt;
+    cur = c1 + 1 == RING ? 0 : c1 + 1;
   }
   if (active) {  // O += V P of the last sub-tile
 #pragma unroll
