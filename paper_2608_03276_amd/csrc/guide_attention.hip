@@ -9,7 +9,7 @@
 // layer, KV head, chunk, group of <= 256 guide rows), eight waves (two per SIMD, so that one
 // wave's exponentials overlap the other's MFMAs), wave w owning rows 32w .. 32w + 31.  The
 // chunk's 32-token sub-tiles of K and V stream through a ring of LDS slots filled by direct
-// global->LDS copies issued several sub-tiles ahead (one barrier per sub-tile), and every
+// global->LDS copies issued several sub-tiles ahead (one barrier per pair of sub-tiles), and every
 // wave reads the whole sub-tile.  Per sub-tile, on v_mfma_f32_32x32x16_bf16:
 //   S^T = K Q^T (tokens on M, rows on N): a lane holds one row and 16 of the 32 tokens (its
 //       partner lane 32 apart holds the other 16), so the row's running maximum and sum stay
@@ -24,6 +24,8 @@
 // are one more chunk, with the causal mask.  A merge kernel combines the chunks.
 #include "tile_common.h"
 #include "tp_internal.h"
+
+#include <type_traits>
 
 namespace tp {
 namespace {
@@ -64,23 +66,64 @@ __device__ inline void copy16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
 }
 
-// Issue this wave's share of the copies of sub-tile rows [t0, t0 + 32) of K and V into the
-// slot at LDS byte `slot` (rows past ntok repeat the last row: finite data the masks drop).
-// The 2 * kTileBytes / 1 KB copies go kCopies to a wave: K's first, then V's.
+// Copy j (0 .. 2 kTileBytes / 1 KB - 1) of a sub-tile, 1 KB: K's first, then V's, kCopies to a
+// wave.  Returns whether it is V's and gives the lane's token in the sub-tile and the byte
+// offset of its swizzled 16-byte piece within that token's row.
 template <int D>
-__device__ inline void copy_subtile(const char* kbase, const char* vbase, int t0, int ntok, uint32_t slot, int wave) {
+__device__ inline bool copy_lane(int j, int& tl, int& piece) {
   using C = Cfg<D>;
   constexpr int kKB = 32 / C::kTokPerKB;  // 1 KB copies per 32-token tile
   const int lane = threadIdx.x & 63;
+  const bool isv = j >= kKB;
+  const int jj = isv ? j - kKB : j;
+  tl = jj * C::kTokPerKB + lane / C::kPieces;
+  piece = ((lane % C::kPieces) ^ (isv ? swzv<D>(tl) : swz<D>(tl))) * 16;
+  return isv;
+}
+
+// Issue this wave's share of the copies of sub-tile rows [t0, t0 + 32) of K and V into the
+// slot at LDS byte `slot` (rows past ntok repeat the last row: finite data the masks drop).
+template <int D>
+__device__ inline void copy_subtile(const char* kbase, const char* vbase, int t0, int ntok, uint32_t slot, int wave) {
 #pragma unroll
   for (int i = 0; i < AttnCfg<D>::kCopies; ++i) {
     const int j = wave * AttnCfg<D>::kCopies + i;  // wave-uniform
-    const bool isv = j >= kKB;
-    const int jj = isv ? j - kKB : j;
-    const int tl = jj * C::kTokPerKB + lane / C::kPieces;
-    const int p = (lane % C::kPieces) ^ (isv ? swzv<D>(tl) : swz<D>(tl));
+    int tl, piece;
+    const bool isv = copy_lane<D>(j, tl, piece);
     const int tok = min(t0 + tl, ntok - 1);
-    copy16((isv ? vbase : kbase) + (uint32_t)tok * C::kRowBytes + p * 16, slot + (uint32_t)j * 1024u);
+    copy16((isv ? vbase : kbase) + (uint32_t)tok * Cfg<D>::kRowBytes + piece, slot + (uint32_t)j * 1024u);
+  }
+}
+
+// The scalar-address form of copy16: the lane's bytes come from sbase + voff, sbase
+// wave-uniform.
+__device__ inline void copy16s(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
+// The lane's offsets for copy_whole, fixed for the kernel.
+template <int D>
+__device__ inline void copy_offsets(uint32_t (&voff)[AttnCfg<D>::kCopies], int wave) {
+#pragma unroll
+  for (int i = 0; i < AttnCfg<D>::kCopies; ++i) {
+    int tl, piece;
+    copy_lane<D>(wave * AttnCfg<D>::kCopies + i, tl, piece);
+    voff[i] = (uint32_t)(tl * Cfg<D>::kRowBytes + piece);
+  }
+}
+
+// copy_subtile for a sub-tile whose 32 rows all exist: no clamp, and the row address is a
+// wave-uniform base plus the lane's fixed offset, so issuing a copy takes no vector work.
+template <int D>
+__device__ inline void copy_whole(const char* kbase, const char* vbase, int t0, const uint32_t (&voff)[AttnCfg<D>::kCopies],
+                                  uint32_t slot, int wave) {
+  constexpr int kKB = 32 / Cfg<D>::kTokPerKB;
+#pragma unroll
+  for (int i = 0; i < AttnCfg<D>::kCopies; ++i) {
+    const int j = wave * AttnCfg<D>::kCopies + i;  // wave-uniform
+    const char* base = (j >= kKB ? vbase : kbase) + (int64_t)t0 * Cfg<D>::kRowBytes;
+    copy16s(voff[i], base, slot + (uint32_t)j * 1024u);
   }
 }
 
@@ -270,6 +313,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   // copies of sub-tiles t + RING - 2 and t + RING - 1 go into the slots of t - 2 and t - 1,
   // and the barrier closing iteration t + 1 follows the landing of sub-tile t + 5 (the last
   // one the next pair reads).
+  uint32_t cvoff[AC::kCopies];
+  copy_offsets<D>(cvoff, wave);
   // prologue: sub-tiles 0 .. RING-3 in flight; 0 .. 3 landed before the loop
   for (int t = 0; t < RING - 2 && t < nsub; ++t)
     copy_subtile<D>(kb, vb, 32 * t, ntok, ring_lds + (uint32_t)(t * AC::kSlotBytes), wave);
@@ -289,48 +334,56 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     if (nsub > 1) read_kfrag<D>(ring + AC::kSlotBytes, kf);
   }
   __builtin_amdgcn_s_waitcnt(0xC07F);  // as at every barrier: no LDS read in flight into the loop
-  // iteration t of the pipeline, with `cur` the slot of sub-tile t
-  const auto iteration = [&](int t, int cur) {
+  // iteration t of the pipeline, with `cur` the slot of sub-tile t: consumes S of sub-tile t
+  // (st) and leaves S of sub-tile t + 1 in sn; FULL marks a sub-tile of the context with all
+  // 32 tokens present and sub-tile t + 2 existing (no mask, no bounds test)
+  const auto iteration = [&](int t, int cur, f32x16& st, f32x16& sn, auto full) {
+    constexpr bool FULL = decltype(full)::value;
     const char* slot = ring + cur * AC::kSlotBytes;
-    // sc[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
-    if (32 * (t + 1) > ntok || u.guide) {
+    // st[i]: token 32 t + (i/4)*8 + (lane/32)*4 + i%4 of the unit, the lane's row
+    if (!FULL && (32 * (t + 1) > ntok || u.guide)) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int tok = 32 * t + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
         const bool seen = tok < ntok && (!u.guide || tok <= jrow);
-        sc[i] = seen ? sc[i] : -INFINITY;
+        st[i] = seen ? st[i] : -INFINITY;
       }
     }
     // S of sub-tile t + 1 (past the end: a repeat of the last sub-tile, never used) and
     // O += V P of sub-tile t - 1, one MFMA of each per step (S first: its chain is
-    // dependent), each step also computing 16 / KS of the exponentials of sub-tile t; the
-    // scheduling barriers keep the steps in this order.
+    // dependent), each step also computing 16 / KS of the exponentials of sub-tile t and
+    // adding those of the step before (an exponential's result is not read right after it);
+    // the scheduling barriers keep the steps in this order.
     static_assert(KS == 2 * NDB, "as many S steps as O steps");
     constexpr int TPS = 16 / KS;  // terms per step
-    f32x16 sn = {};
     float p[16];
-    float e[4] = {0.f, 0.f, 0.f, 0.f};
+    float e[4] = {-0.f, -0.f, -0.f, -0.f};  // -0 + x == x: the first additions fold away
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, sn, 0, 0, 0);
+      sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, s == 0 ? (f32x16){} : sn, 0, 0, 0);
       ot[s % NDB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[s % NDB][s / NDB].v, pb[s / NDB], ot[s % NDB], 0, 0, 0);
 #pragma unroll
       for (int j = 0; j < TPS; ++j) {
         const int i = TPS * s + j;
-        p[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], a.c, -m));
-        e[i & 3] += p[i];
+        p[i] = __builtin_amdgcn_exp2f(fmaf(st[i], a.c, -m));
+        if (s > 0) e[(i - TPS) & 3] += p[i - TPS];
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
+      if (s > 0)
+        __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
+      else
+        __builtin_amdgcn_sched_group_barrier(0x002, TPS, 0);
       __builtin_amdgcn_sched_group_barrier(0x400, TPS, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int j = 0; j < TPS; ++j) e[(16 - TPS + j) & 3] += p[16 - TPS + j];
     float ps = (e[0] + e[1]) + (e[2] + e[3]);
     const bool big = !(ps < kAttnLazyLimit);
     const uint64_t bal = __builtin_amdgcn_ballot_w64(big);
     if (bal) {
       const uint32_t pair = (uint32_t)bal | (uint32_t)(bal >> 32);
-      if ((pair >> (lane & 31)) & 1u) raise_max<NDB>(sc, a.c, m, lsum, ot, p, ps);
+      if ((pair >> (lane & 31)) & 1u) raise_max<NDB>(st, a.c, m, lsum, ot, p, ps);
     }
     lsum += ps;
 #pragma unroll
@@ -343,14 +396,36 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) vf[db][s2] = read_vfrag<D>(slot + AC::kTileBytes, db, s2);
-    if (t + 2 < nsub) {
+    if (FULL || t + 2 < nsub) {
       const int k2 = cur + 2 >= RING ? cur + 2 - RING : cur + 2;
       read_kfrag<D>(ring + k2 * AC::kSlotBytes, kf);
     }
-    sc = sn;
   };
+  using Full = std::integral_constant<bool, true>;
+  using Any = std::integral_constant<bool, false>;
+  f32x16 sc2;  // S of the odd sub-tile of a pair
   int cur = 0;  // slot of sub-tile t
-  for (int t = 0; t < nsub; t += 2) {
+  int t = 0;
+  // Pairs whose copies are whole context sub-tiles (t + RING - 1 <= nsub - 2): no bounds
+  // tests, a fixed wait and copies addressed from a wave-uniform base.
+  if (!u.guide) {
+    for (; t + RING < nsub; t += 2) {
+      const int f1 = cur >= 2 ? cur - 2 : cur + RING - 2;
+      copy_whole<D>(kb, vb, 32 * (t + RING - 2), cvoff, ring_lds + (uint32_t)(f1 * AC::kSlotBytes), wave);
+      const int f2 = cur >= 1 ? cur - 1 : cur + RING - 1;
+      copy_whole<D>(kb, vb, 32 * (t + RING - 1), cvoff, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
+      const int c1 = cur + 1 == RING ? 0 : cur + 1;
+      if (active) {
+        iteration(t, cur, sc, sc2, Full{});
+        iteration(t + 1, c1, sc2, sc, Full{});
+      }
+      // sub-tile t + 5 has landed for every wave; those of t + 6 .. t + RING - 1 may not have
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RING - 6) * AC::kCopies) : "memory");
+      ring_barrier();
+      cur = c1 + 1 == RING ? 0 : c1 + 1;
+    }
+  }
+  for (; t < nsub; t += 2) {
     // the slots of sub-tiles t - 2 and t - 1, read before the last barrier
     const int f1 = cur >= 2 ? cur - 2 : cur + RING - 2;
     const int f2 = cur >= 1 ? cur - 1 : cur + RING - 1;
@@ -360,8 +435,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
       copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
     const int c1 = cur + 1 == RING ? 0 : cur + 1;
     if (active) {
-      iteration(t, cur);
-      if (t + 1 < nsub) iteration(t + 1, c1);
+      iteration(t, cur, sc, sc2, Any{});
+      if (t + 1 < nsub) iteration(t + 1, c1, sc2, sc, Any{});
     }
     // sub-tile t + 5 has landed for every wave; copies of t + 6 .. may stay in flight
     wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 5), 0));
