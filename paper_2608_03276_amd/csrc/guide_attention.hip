@@ -304,9 +304,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
       (int)(uintptr_t)(__attribute__((address_space(3))) char*)ring);
   // Software pipeline: iteration t issues, interleaved with the exponentials of sub-tile t,
   // the MFMAs of S for sub-tile t + 1 and of O += V P for sub-tile t - 1 (neither depends on
-  // those exponentials, so the matrix pipe has work while the vector ALU computes them); then
-  // it reads the V fragments of sub-tile t and the K fragments of sub-tile t + 2, so every
-  // operand of the next iteration is in registers when it starts.  A raise of the maximum in
+  // those exponentials, so the matrix pipe has work while the vector ALU computes them).  Each
+  // step refills the fragment registers its two MFMAs have just consumed with the next
+  // iteration's (V of sub-tile t, K of sub-tile t + 2), so those reads have most of an
+  // iteration to land before they are used.  A raise of the maximum in
   // iteration t rescales O after sub-tile t - 1 has been added with the old maximum.
   // Sub-tile x lives in ring slot x mod RING; its last reads are those of iteration x.  The
   // iterations run in pairs (t even, t + 1) with one barrier after each pair: after it, the
@@ -352,12 +353,17 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     // S of sub-tile t + 1 (past the end: a repeat of the last sub-tile, never used) and
     // O += V P of sub-tile t - 1, one MFMA of each per step (S first: its chain is
     // dependent), each step also computing 16 / KS of the exponentials of sub-tile t and
-    // adding those of the step before (an exponential's result is not read right after it);
-    // the scheduling barriers keep the steps in this order.
+    // adding those of the step before (an exponential's result is not read right after it),
+    // then reading the fragments of the next iteration into the registers just consumed; the
+    // scheduling barriers keep the steps in this order.
     static_assert(KS == 2 * NDB, "as many S steps as O steps");
     constexpr int TPS = 16 / KS;  // terms per step
     float p[16];
     float e[4] = {-0.f, -0.f, -0.f, -0.f};  // -0 + x == x: the first additions fold away
+    const bool kread = FULL || t + 2 < nsub;
+    const int k2 = cur + 2 >= RING ? cur + 2 - RING : cur + 2;
+    const char* kslot = ring + k2 * AC::kSlotBytes;
+    const char* vtile = slot + AC::kTileBytes;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf[s].v, s == 0 ? (f32x16){} : sn, 0, 0, 0);
@@ -368,12 +374,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
         p[i] = __builtin_amdgcn_exp2f(fmaf(st[i], a.c, -m));
         if (s > 0) e[(i - TPS) & 3] += p[i - TPS];
       }
+      // refill the fragments this step's MFMAs consumed: V of sub-tile t, K of sub-tile t + 2
+      vf[s % NDB][s / NDB] = read_vfrag<D>(vtile, s % NDB, s / NDB);
+      if (kread) read_kfrag_step<D>(kslot, kf[s], s);
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       if (s > 0)
         __builtin_amdgcn_sched_group_barrier(0x002, TPS * 2, 0);
       else
         __builtin_amdgcn_sched_group_barrier(0x002, TPS, 0);
       __builtin_amdgcn_sched_group_barrier(0x400, TPS, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
@@ -390,16 +400,6 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
-    // the next iteration's operands (landed at the last barrier): V of sub-tile t, the K
-    // fragments of sub-tile t + 2
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) vf[db][s2] = read_vfrag<D>(slot + AC::kTileBytes, db, s2);
-    if (FULL || t + 2 < nsub) {
-      const int k2 = cur + 2 >= RING ? cur + 2 - RING : cur + 2;
-      read_kfrag<D>(ring + k2 * AC::kSlotBytes, kf);
-    }
   };
   using Full = std::integral_constant<bool, true>;
   using Any = std::integral_constant<bool, false>;

@@ -39,18 +39,21 @@ __device__ inline int swz(int tl) {
   return D == 128 ? (tl & 15) : ((tl >> 1) & 7);
 }
 
-// K fragment of the staged sub-tile: token lane%32, the d-columns of this half-wave.
+// K fragment of the staged sub-tile for MFMA k-step s: token lane%32, the d-columns of this
+// half-wave.
 template <int D>
-__device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) {
+__device__ inline void read_kfrag_step(const char* kbuf, Frag& f, int s) {
   using C = Cfg<D>;
   const int lane = threadIdx.x & 63;
   const int tl = lane & 31;
-  const char* row = kbuf + tl * C::kRowBytes;
+  const int p = (lane >> 5) * (C::kPieces / 2) + s;
+  f.u = *(const uint4*)(kbuf + tl * C::kRowBytes + ((p ^ swz<D>(tl)) * 16));
+}
+
+template <int D>
+__device__ inline void read_kfrag(const char* kbuf, Frag (&kf)[Cfg<D>::kSteps]) {
 #pragma unroll
-  for (int s = 0; s < C::kSteps; ++s) {
-    const int p = (lane >> 5) * (C::kPieces / 2) + s;
-    kf[s].u = *(const uint4*)(row + ((p ^ swz<D>(tl)) * 16));
-  }
+  for (int s = 0; s < Cfg<D>::kSteps; ++s) read_kfrag_step<D>(kbuf, kf[s], s);
 }
 
 // The largest of the 16 accumulator values a lane holds.
