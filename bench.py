@@ -31,7 +31,8 @@ KERNEL_SOURCES = {"k_guide_stats": ["guide_scores.hip", "tile_common.h", "tp_int
                   "k_guide_lse": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
                   "k_guide_attn": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
                   "k_guide_pool": ["guide_scores.hip", "tile_common.h", "tp_internal.h"],
-                  "k_guide_fwd": ["guide_attention.hip", "tile_common.h", "tp_internal.h"],
+                  "k_guide_fwd": ["guide_attention.hip", "tile_common.h", "quant_row.h", "quant_recip_table.h",
+                                  "tp_internal.h"],
                   # the rows each step-2 launch takes are set by tp_evict
                   "k_quantize": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
                   "k_quantize_lean": ["quantize.hip", "quant_row.h", "quant_recip_table.h", "tp_internal.h", "abi.cpp"],
@@ -333,9 +334,10 @@ def main():
                     help="guide rows' log-normalisers supplied (as a prefill attention kernel exports them): "
                          "score pass 1 is skipped")
     ap.add_argument("--prefill-attention", action="store_true",
-                    help="the prefill-integrated path: one step is the guide rows' prefill attention "
-                         "(tp_guide_attention over the context and the guide's own keys and values: outputs and "
-                         "normalisers) followed by tp_evict with those normalisers (a secondary line)")
+                    help="the prefill-integrated path: one step is the guide rows' prefill attention with step 2 "
+                         "from the same sweep over V (tp_guide_attention_quantize over the context and the guide's "
+                         "own keys and values: outputs, normalisers, V scales and codes) followed by tp_evict with "
+                         "those normalisers, scales and codes (a secondary line)")
     ap.add_argument("--no-full-codes", action="store_true",
                     help="step 2 writes the scales only and the compaction quantises the kept V rows "
                          "(the codes of evicted rows are never written)")
@@ -349,6 +351,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
+    if args.prefill_attention and args.no_full_codes:
+        ap.error("--prefill-attention writes every token's codes with the attention: drop --no-full-codes")
     if args.gpus != 1:
         print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); the path shards by "
               f"(layer, KV head, sequence) with no communication, so each GPU would run it on its own share.",
@@ -380,7 +384,7 @@ def main():
     kg = SD.device_guide_keys(w) if (args.guide_keys or args.prefill_attention) else None
     vg = SD.device_guide_values(w) if args.prefill_attention else None
     lse = prefill_lse(w, q, k, kg) if args.given_lse else None
-    if args.prefill_attention:  # written by tp_guide_attention inside every step
+    if args.prefill_attention:  # written by tp_guide_attention_quantize inside every step
         lse = torch.empty(w.L * w.Hq * w.g_tot, dtype=torch.float32, device="cuda")
         o_guide = torch.empty(w.L * w.Hq * w.g_tot * w.d, dtype=torch.float32, device="cuda")
     kg_arg = None if lse is not None else kg
@@ -396,10 +400,11 @@ def main():
         if args.prefill_attention:
             if att is not None:
                 att[0].record()
-            B.tp_guide_attention(d, bt, q, k, v, w.softmax_scale, o_guide, lse, ws_attn, k_guide=kg, v_guide=vg)
+            B.tp_guide_attention_quantize(d, bt, q, k, v, w.softmax_scale, w.qfmt, w.bits, o_guide, lse,
+                                          bufs.scales, bufs.v_q, ws_attn, k_guide=kg, v_guide=vg)
             if att is not None:
                 att[1].record()
-        B.tp_evict(d, bt, q, k, v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
+        B.tp_evict(d, bt, q, k, None if args.prefill_attention else v, w.softmax_scale, w.pool_k, w.qfmt, w.bits, w.rule, w.keep_ratio or 0.0,
                    w.keep_budget or 0, ko, bufs.s_key, bufs.scales, None if args.no_full_codes else bufs.v_q,
                    bufs.s_comb, bufs.kept_idx, bufs.k_c,
                    bufs.v_q_c, bufs.scales_c, bufs.ws_evict, events=ev, k_guide=kg_arg, guide_lse=lse)
@@ -434,7 +439,8 @@ def main():
         stages[4] = "k_guide_pool"
     stage_ms = {n: statistics.median(e[j].elapsed_time(e[j + 1]) for e in evs) for j, n in enumerate(stages)}
     stage_ms.pop("pass1_skipped", None)
-    if args.prefill_attention:
+    if args.prefill_attention:  # step 2 ran inside the attention: no kernel between its events
+        stage_ms.pop("k_quantize")
         stage_ms = dict({"k_guide_fwd": statistics.median(a[0].elapsed_time(a[1]) for a in atts)}, **stage_ms)
     timing = {"protocol": f"median of {args.steps} steps, each timed by events at its start and end on the "
                           f"stream it runs on, after {args.warmup} untimed warm-up steps; a {FLUSH_BYTES >> 20} MB "
@@ -455,6 +461,8 @@ def main():
                                     if args.prefill_attention else 0)
     per["k_guide_fwd"] = (2 * w.L * w.Hkv * w.n_tot * w.d * 2 + w.L * w.Hq * w.g_tot * w.d * (2 + 4)
                           + 2 * w.L * w.Hkv * w.g_tot * w.d * 2)  # K, V, Q and guide K/V read; O written
+    if args.prefill_attention:  # with step 2: V's codes and scales written
+        per["k_guide_fwd"] += w.L * w.Hkv * w.n_tot * (B.row_bytes(w.qfmt, w.bits, w.d) + 4)
 
     def roofline_of(kern):
         # the roof is whichever of HBM bytes and matrix flops takes longer at its peak; the
@@ -502,7 +510,8 @@ def main():
         "data": "synthetic (seeded SplitMix64/Box-Muller draws of the workload's shapes and distributions)",
         "config": {"workload": w.describe()
                    + (", the guide rows' prefill attention (context and guide keys: outputs and normalisers) "
-                      "followed by the eviction from its normalisers" if args.prefill_attention else "")
+                      "with V's scales and codes from the same sweep, followed by the eviction from those"
+                      if args.prefill_attention else "")
                    + (", guide keys in the normaliser" if kg is not None and not args.prefill_attention else "")
                    + (", row normalisers supplied by the prefill (score pass 1 skipped)"
                       if args.given_lse else "")

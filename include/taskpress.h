@@ -185,6 +185,23 @@ tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const v
                              float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * tp_guide_attention together with step 2 (Eq. 2, Sec. 3.3) from the one sweep over V: the
+ * V tiles the attention stages are also quantised, so the prefill's quantised cache and the
+ * value scores come from the attention's own read of V (the paper takes the scales as
+ * already computed by the cache's quantisation).  Outputs o_guide and guide_lse exactly as
+ * tp_guide_attention; scales and v_q exactly (bit for bit) as tp_quantize_v_scales with the
+ * same qfmt and bits, for every context token of the batch.  v_q must be non-NULL
+ * (TP_ERR_NULL otherwise).  tp_evict then takes v = NULL with these scales and codes.
+ * Same workspace as tp_guide_attention.  Errors as for tp_guide_attention and
+ * tp_quantize_v_scales.
+ */
+tp_status tp_guide_attention_quantize(const tp_dims* dims, const tp_batch* batch, const void* q_guide,
+                                      const void* k, const void* v, const void* k_guide, const void* v_guide,
+                                      float softmax_scale, int32_t qfmt, int32_t bits, float* o_guide,
+                                      float* guide_lse, float* scales, void* v_q, void* workspace, size_t ws_bytes,
+                                      void* stream);
+
+/*
  * Step 2 — value score of Eq. 2 (Sec. 3.3), fused with per-token quantisation of V
  * (KIVI-style per-token scheme cited in Sec. 3.3; int4 cache of Sec. 4 setup):
  *   gamma[l][h][t] = fl32( max_c |v[l][h][t][c]| / qmax )
@@ -303,6 +320,9 @@ typedef struct tp_profile {
  * scales_out.  With v_q == NULL step 2 computes the scales only and the compaction
  * quantises the kept V rows itself (tp_compact_quantize_kv): the compact cache is the same
  * and the codes of the evicted rows are never written.
+ * v == NULL: step 2 has been done (tp_guide_attention_quantize, or tp_quantize_v_scales):
+ * scales and v_q are inputs holding its results for qfmt and bits (both non-NULL, else
+ * TP_ERR_NULL), and everything runs on `stream` (no second stream, no library state).
  * workspace: >= tp_workspace_size(TP_FN_EVICT, ...) bytes, 256-byte aligned (the score
  * pass's workspace followed by the selection's).
  * Step 2 of most V rows runs on a second stream of the library's: 2/5 concurrently with each

@@ -22,7 +22,8 @@ TP_MAX_BATCH = 64
 TP_EVICT_EVENTS = 8
 
 EXPORTED = ("tp_version", "tp_status_string", "tp_last_error", "tp_keep_count", "tp_workspace_size",
-            "tp_guide_scores", "tp_guide_scores_lse", "tp_guide_attention", "tp_quantize_v_scales",
+            "tp_guide_scores", "tp_guide_scores_lse", "tp_guide_attention", "tp_guide_attention_quantize",
+            "tp_quantize_v_scales",
             "tp_combine_select_topk",
             "tp_combine_select_topk_static", "tp_compact_kv", "tp_compact_quantize_kv", "tp_evict")
 TP_STATIC_SCRATCH_BYTES = 64 << 20
@@ -115,6 +116,9 @@ def load():
     lib.tp_guide_scores_lse.argtypes = [pd, pb, P, P, P, ctypes.c_float, ctypes.c_int32, P, P, ctypes.c_size_t, P]
     lib.tp_guide_attention.restype = ctypes.c_int32
     lib.tp_guide_attention.argtypes = [pd, pb, P, P, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
+    lib.tp_guide_attention_quantize.restype = ctypes.c_int32
+    lib.tp_guide_attention_quantize.argtypes = [pd, pb, P, P, P, P, P, ctypes.c_float, ctypes.c_int32,
+                                                ctypes.c_int32, P, P, P, P, P, ctypes.c_size_t, P]
     lib.tp_quantize_v_scales.restype = ctypes.c_int32
     lib.tp_quantize_v_scales.argtypes = [pd, pb, P, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.tp_combine_select_topk.restype = ctypes.c_int32
@@ -233,6 +237,30 @@ def tp_guide_attention(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: fl
     _check(load().tp_guide_attention(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k), _ptr(v),
                                      _ptr(k_guide), _ptr(v_guide), float(softmax_scale), _ptr(o_guide),
                                      _ptr(guide_lse), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def tp_guide_attention_quantize(d: TpDims, batch: Batch, q_guide, k, v, softmax_scale: float, qfmt: int,
+                                bits: int, o_guide, guide_lse, scales, v_q, workspace=None, stream=None,
+                                k_guide=None, v_guide=None):
+    """tp_guide_attention plus step 2 from the same sweep over V: scales fp32 [L][Hkv][N_tot]
+    and the codes v_q [L][Hkv][N_tot][row_bytes], as tp_quantize_v_scales writes them."""
+    L, Hq, Hkv, D = d.num_layers, d.num_q_heads, d.num_kv_heads, d.head_dim
+    _need(q_guide, L * Hq * batch.g_tot * D * 2, "q_guide")
+    _need(k, L * Hkv * batch.n_tot * D * 2, "k")
+    _need(v, L * Hkv * batch.n_tot * D * 2, "v")
+    _need(k_guide, L * Hkv * batch.g_tot * D * 2, "k_guide")
+    _need(v_guide, L * Hkv * batch.g_tot * D * 2, "v_guide")
+    _need(o_guide, L * Hq * batch.g_tot * D * 4, "o_guide")
+    _need(guide_lse, L * Hq * batch.g_tot * 4, "guide_lse")
+    _need(scales, L * Hkv * batch.n_tot * 4, "scales")
+    _need(v_q, L * Hkv * batch.n_tot * row_bytes(qfmt, bits, D), "v_q")
+    if workspace is None:
+        workspace = torch.empty(tp_workspace_size(TP_FN_GUIDE_ATTENTION, d, batch), dtype=torch.uint8,
+                                device=q_guide.device)
+    _check(load().tp_guide_attention_quantize(ctypes.byref(d), ctypes.byref(batch.c), _ptr(q_guide), _ptr(k),
+                                              _ptr(v), _ptr(k_guide), _ptr(v_guide), float(softmax_scale),
+                                              int(qfmt), int(bits), _ptr(o_guide), _ptr(guide_lse), _ptr(scales),
+                                              _ptr(v_q), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def row_bytes(qfmt: int, bits: int, head_dim: int) -> int:

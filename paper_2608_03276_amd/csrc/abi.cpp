@@ -530,9 +530,13 @@ tp_status tp_guide_scores_lse(const tp_dims* dims, const tp_batch* batch, const 
   return ok();
 }
 
-tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
-                             const void* v, const void* k_guide, const void* v_guide, float softmax_scale,
-                             float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+// The guide rows' attention; with qa (step 2 already validated) the kernel also quantises V.
+static tp_status guide_attention(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                                 const void* v, const void* k_guide, const void* v_guide, float softmax_scale,
+                                 float* o_guide, float* guide_lse, const tp::QuantArgs* qa, void* workspace,
+                                 size_t ws_bytes, void* stream) {
   tp_status s = check_dims(dims);
   if (s != TP_OK) return s;
   s = check_batch(dims, batch, true);
@@ -585,9 +589,39 @@ tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const v
     return fail(TP_ERR_UNSUPPORTED, "context or guide too long for one launch");
   a.nchunk_max = (int32_t)nchunk;
   a.nrg_max = (int32_t)nrg;
+  if (qa) {
+    a.scales = qa->scales;
+    a.vq = qa->vq;
+    a.qfmt = qa->qfmt;
+    a.bits = qa->bits;
+    a.qmax = qa->qmax;
+    a.ro = qa->ro;
+  }
   const hipError_t e = tp::launch_guide_attention(a, dims->head_dim, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tp_guide_attention launch");
   return ok();
+}
+
+extern "C" {
+
+tp_status tp_guide_attention(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
+                             const void* v, const void* k_guide, const void* v_guide, float softmax_scale,
+                             float* o_guide, float* guide_lse, void* workspace, size_t ws_bytes, void* stream) {
+  return guide_attention(dims, batch, q_guide, k, v, k_guide, v_guide, softmax_scale, o_guide, guide_lse, nullptr,
+                         workspace, ws_bytes, stream);
+}
+
+tp_status tp_guide_attention_quantize(const tp_dims* dims, const tp_batch* batch, const void* q_guide,
+                                      const void* k, const void* v, const void* k_guide, const void* v_guide,
+                                      float softmax_scale, int32_t qfmt, int32_t bits, float* o_guide,
+                                      float* guide_lse, float* scales, void* v_q, void* workspace, size_t ws_bytes,
+                                      void* stream) {
+  tp::QuantArgs qa;
+  const tp_status s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);
+  if (s != TP_OK) return s;
+  if (!v_q) return fail(TP_ERR_NULL, "v_q must be non-NULL (the codes are written with the scales)");
+  return guide_attention(dims, batch, q_guide, k, v, k_guide, v_guide, softmax_scale, o_guide, guide_lse, &qa,
+                         workspace, ws_bytes, stream);
 }
 
 tp_status tp_quantize_v_scales(const tp_dims* dims, const tp_batch* batch, const void* v, int32_t qfmt,
@@ -660,6 +694,36 @@ tp_status tp_compact_quantize_kv(const tp_dims* dims, const tp_batch* batch, con
   return ok();
 }
 
+}  // extern "C"
+
+// tp_evict when step 2 was done beforehand: steps 1, 3 and 4 on the caller's stream only.
+// Event [3] (after step 2) follows [2] with no kernel between them.
+static tp_status evict_without_step2(const tp::GuideArgs& ga, const tp::SelectArgs& sa, const tp::CompactArgs& ca,
+                                     bool fuse_pool, const tp_dims* dims, hipStream_t st, hipEvent_t* ev) {
+  struct Rec {
+    hipEvent_t done;
+    hipStream_t st;
+  } rec{ev ? ev[3] : nullptr, st};
+  auto mark = [](void* c) -> hipError_t {
+    const Rec* r = (const Rec*)c;
+    return r->done ? hipEventRecord(r->done, r->st) : hipSuccess;
+  };
+  const int segs = dims->num_layers * dims->num_kv_heads;
+  hipEvent_t gev[4] = {ev ? ev[1] : nullptr, ev ? ev[2] : nullptr, ev ? ev[4] : nullptr,
+                       ev && !fuse_pool ? ev[5] : nullptr};
+  hipError_t e = hipSuccess;
+  if (ev) e = hipEventRecord(ev[0], st);
+  if (e == hipSuccess) e = tp::launch_guide_scores(ga, dims->head_dim, st, ev ? gev : nullptr, mark, &rec);
+  if (e == hipSuccess) e = tp::launch_select(sa, segs, st, ev && fuse_pool ? ev[5] : nullptr);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[6], st);
+  if (e == hipSuccess) e = tp::launch_compact(ca, segs, dims->head_dim, st);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[7], st);
+  if (e != hipSuccess) return hip_fail(e, "tp_evict launch");
+  return ok();
+}
+
+extern "C" {
+
 tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_guide, const void* k,
                    const void* k_guide, const float* guide_lse, const void* v, float softmax_scale, int32_t pool_k, int32_t qfmt, int32_t bits, int32_t rule, double keep_ratio,
                    int64_t keep_budget, const int64_t* kept_offsets, float* s_key, float* scales, void* v_q,
@@ -682,9 +746,16 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
   tp::GuideArgs ga;
   s = prepare_guide(dims, batch, q_guide, k, k_guide, guide_lse, softmax_scale, pool_k, s_key, workspace, gws, ga);
   if (s != TP_OK) return s;
+  // v == NULL: step 2 is done (tp_guide_attention_quantize): scales and v_q are its results
+  const bool step2 = v != nullptr;
   tp::QuantArgs qa;
-  s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);
-  if (s != TP_OK) return s;
+  memset(&qa, 0, sizeof qa);
+  if (step2) {
+    s = prepare_quant(dims, batch, v, qfmt, bits, scales, v_q, qa);
+    if (s != TP_OK) return s;
+  } else if (!scales || !v_q) {
+    return fail(TP_ERR_NULL, "without v, scales and v_q must hold step 2's results");
+  }
   tp::SelectArgs sa;
   s = prepare_select(dims, batch, s_key, scales, rule, keep_ratio, keep_budget, kept_offsets, kept_idx, s_out,
                      (char*)workspace + gws, ews - gws, sa);
@@ -713,6 +784,7 @@ tp_status tp_evict(const tp_dims* dims, const tp_batch* batch, const void* q_gui
 
   const hipStream_t st = (hipStream_t)stream;
   hipEvent_t* ev = (profile && profile->num_events) ? (hipEvent_t*)profile->events : nullptr;
+  if (!step2) return evict_without_step2(ga, sa, ca, fuse_pool, dims, st, ev);
   AuxStream* aux = nullptr;
   s = aux_stream_for(st, aux);
   if (s != TP_OK) return s;

@@ -22,6 +22,7 @@
 //       operand comes from the token-major V sub-tile through transposing LDS reads.
 // Each workgroup writes its rows' partial (max, sum) and unnormalised O; the guide's own keys
 // are one more chunk, with the causal mask.  A merge kernel combines the chunks.
+#include "quant_row.h"
 #include "tile_common.h"
 #include "tp_internal.h"
 
@@ -33,6 +34,7 @@ namespace {
 constexpr int kAttnThreads = 512;  // 8 waves, two per SIMD, 32 rows each
 constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr float kAttnLazyLimit = 4294967296.0f;  // 2^32: a lane's 16 terms against a stale maximum
+constexpr int kAttnNoQuant = -1;  // the instance that leaves V's step 2 to its own kernel
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -253,7 +255,11 @@ __device__ inline bool attn_unit(const AttnArgs& a, AttnUnit& u) {
   return false;
 }
 
-template <int D>
+// QK: kAttnNoQuant, or the QKind of the codes when the kernel also performs step 2 (Eq. 2)
+// on the V sub-tiles it stages: the workgroup of a context chunk's first row group quantises
+// each token row of the chunk once, from LDS (the arithmetic of quant_row.h, bit-identical to
+// the quantisation kernel's).
+template <int D, int QK>
 __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   AttnUnit u;
   if (!attn_unit(a, u)) return;
@@ -262,7 +268,13 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   constexpr int KS = C::kSteps;
   constexpr int NDB = D / 32;  // 32-wide d-blocks of O
   constexpr int RING = AC::kRing;
-  __shared__ __attribute__((aligned(1024))) char ring[RING * AC::kSlotBytes];
+  constexpr bool QUANT = QK != kAttnNoQuant;
+  constexpr int QKC = QUANT ? QK : 0;
+  constexpr int LPT = D / 8;     // lanes per V row in the quantisation
+  constexpr int RPW = 64 / LPT;  // rows per wave
+  // the ring, then (QUANT) the quantisation tables
+  __shared__ __attribute__((aligned(1024))) char ring[RING * AC::kSlotBytes + (QUANT ? sizeof(QuantTables) : 0)];
+  QuantTables& tab = *(QuantTables*)(ring + RING * AC::kSlotBytes);
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const bool active = 32 * wave < u.nrows;
@@ -316,6 +328,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   // one the next pair reads).
   uint32_t cvoff[AC::kCopies];
   copy_offsets<D>(cvoff, wave);
+  if (QUANT) build_tables(tab, a.qmax, a.ro.off);  // read after the prologue's barrier
   // prologue: sub-tiles 0 .. RING-3 in flight; 0 .. 3 landed before the loop
   for (int t = 0; t < RING - 2 && t < nsub; ++t)
     copy_subtile<D>(kb, vb, 32 * t, ntok, ring_lds + (uint32_t)(t * AC::kSlotBytes), wave);
@@ -401,6 +414,28 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
   };
+  // Step 2 of the token rows of sub-tile x (ring slot sl), RPW rows per wave: read from the
+  // staged V tile, quantised, scale and codes stored.  Only the workgroup of the chunk's
+  // first row group does this, in waves 0 .. 32 / RPW - 1.  Its stores are vector-memory
+  // operations like the ring's copies and may complete out of order with them, so a wave
+  // that quantises waits for all of its memory operations at each barrier (vmcnt(0)), which
+  // leaves each pair's copies the pair's duration to land.
+  const bool qwave = QUANT && !u.guide && u.rg == 0 && wave < 32 / RPW;
+  const QuantFmt qfmt{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
+  const int64_t qrow0 = (int64_t)u.seg * a.n_tot + u.n0 + (int64_t)u.chunk * a.chunk;
+  const auto quant_sub = [&](int x, int sl) {
+    const int tl = wave * RPW + lane / LPT;
+    const int p = lane % LPT;
+    const char* vt = ring + sl * AC::kSlotBytes + AC::kTileBytes;
+    const uint4 xv = *(const uint4*)(vt + tl * C::kRowBytes + ((p ^ swzv<D>(tl)) << 4));
+    uint2 cd;
+    const float gamma = quant_piece<LPT, QKC>(xv, tab, qfmt, cd);
+    const int tok = 32 * x + tl;
+    if (tok < ntok) {  // rows past the chunk's end repeat its last row
+      if (p == 0) a.scales[qrow0 + tok] = gamma;
+      store_codes<D, QKC>(a.vq, qrow0 + tok, p, cd);
+    }
+  };
   using Full = std::integral_constant<bool, true>;
   using Any = std::integral_constant<bool, false>;
   f32x16 sc2;  // S of the odd sub-tile of a pair
@@ -415,12 +450,19 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
       const int f2 = cur >= 1 ? cur - 1 : cur + RING - 1;
       copy_whole<D>(kb, vb, 32 * (t + RING - 1), cvoff, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
       const int c1 = cur + 1 == RING ? 0 : cur + 1;
+      if (qwave) {
+        quant_sub(t, cur);
+        quant_sub(t + 1, c1);
+      }
       if (active) {
         iteration(t, cur, sc, sc2, Full{});
         iteration(t + 1, c1, sc2, sc, Full{});
       }
       // sub-tile t + 5 has landed for every wave; those of t + 6 .. t + RING - 1 may not have
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RING - 6) * AC::kCopies) : "memory");
+      if (QUANT)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RING - 6) * AC::kCopies) : "memory");
       ring_barrier();
       cur = c1 + 1 == RING ? 0 : c1 + 1;
     }
@@ -434,12 +476,19 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     if (t + RING - 1 < nsub)
       copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
     const int c1 = cur + 1 == RING ? 0 : cur + 1;
+    if (qwave) {
+      quant_sub(t, cur);
+      if (t + 1 < nsub) quant_sub(t + 1, c1);
+    }
     if (active) {
       iteration(t, cur, sc, sc2, Any{});
       if (t + 1 < nsub) iteration(t + 1, c1, sc2, sc, Any{});
     }
     // sub-tile t + 5 has landed for every wave; copies of t + 6 .. may stay in flight
-    wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 5), 0));
+    if (QUANT)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else
+      wait_copies_but<AC::kCopies>(max(min(t + RING - 1, nsub - 1) - (t + 5), 0));
     ring_barrier();
     cur = c1 + 1 == RING ? 0 : c1 + 1;
   }
@@ -502,6 +551,27 @@ __global__ __launch_bounds__(256) void k_guide_fwd_merge(AttnArgs a) {
   if (lane == 0) a.lse[grow] = (mstar + log2f(tot)) * 0.69314718055994531f;
 }
 
+template <int D>
+void launch_fwd(const AttnArgs& a, dim3 grid, hipStream_t stream) {
+  if (a.vq == nullptr) {
+    hipLaunchKernelGGL((k_guide_fwd<D, kAttnNoQuant>), grid, dim3(kAttnThreads), 0, stream, a);
+    return;
+  }
+  switch (qkind_of(a.qfmt, a.bits)) {
+    case kQInt8:
+      hipLaunchKernelGGL((k_guide_fwd<D, kQInt8>), grid, dim3(kAttnThreads), 0, stream, a);
+      break;
+    case kQByte:
+      hipLaunchKernelGGL((k_guide_fwd<D, kQByte>), grid, dim3(kAttnThreads), 0, stream, a);
+      break;
+    case kQNibble:
+      hipLaunchKernelGGL((k_guide_fwd<D, kQNibble>), grid, dim3(kAttnThreads), 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((k_guide_fwd<D, kQE4M3>), grid, dim3(kAttnThreads), 0, stream, a);
+  }
+}
+
 }  // namespace
 
 AttnWorkspace attn_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, int32_t head_dim, const int64_t* ctx_off,
@@ -529,10 +599,10 @@ hipError_t launch_guide_attention(const AttnArgs& a, int head_dim, hipStream_t s
                   (unsigned)(a.bt.batch * a.nrg_max));
   const dim3 mgrid((unsigned)((a.L * a.Hq * max_gb + 3) / 4), (unsigned)a.bt.batch);
   if (head_dim == 128) {
-    hipLaunchKernelGGL(k_guide_fwd<128>, grid, dim3(kAttnThreads), 0, stream, a);
+    launch_fwd<128>(a, grid, stream);
     hipLaunchKernelGGL(k_guide_fwd_merge<128>, mgrid, dim3(256), 0, stream, a);
   } else {
-    hipLaunchKernelGGL(k_guide_fwd<64>, grid, dim3(kAttnThreads), 0, stream, a);
+    launch_fwd<64>(a, grid, stream);
     hipLaunchKernelGGL(k_guide_fwd_merge<64>, mgrid, dim3(256), 0, stream, a);
   }
   return hipGetLastError();

@@ -73,43 +73,6 @@ typedef hipError_t (*GuideBetween)(void* ctx);
 hipError_t launch_guide_scores(const GuideArgs& a, int head_dim, hipStream_t stream, hipEvent_t* ev,
                                GuideBetween between = nullptr, void* ctx = nullptr);
 
-// ---------------------------------------------------------------- guide rows' prefill attention
-// Context tokens per workgroup of the guide rows' attention: 32768 when every sequence has at
-// least 131072 (fewer partial outputs to merge), else 8192.
-constexpr int kAttnChunkSmall = 8192;
-constexpr int kAttnChunkLarge = 32768;
-inline int32_t attn_chunk_tokens(const int64_t* ctx_off, int32_t batch) {
-  for (int b = 0; b < batch; ++b)
-    if (ctx_off[b + 1] - ctx_off[b] < 131072) return kAttnChunkSmall;
-  return kAttnChunkLarge;
-}
-
-struct AttnArgs {
-  const uint16_t* q;   // bf16 [L][Hq][G_tot][d]
-  const uint16_t* k;   // bf16 [L][Hkv][N_tot][d]
-  const uint16_t* v;   // bf16 [L][Hkv][N_tot][d]
-  const uint16_t* kg;  // bf16 [L][Hkv][G_tot][d] the guide tokens' keys, or nullptr
-  const uint16_t* vg;  // bf16 [L][Hkv][G_tot][d] their values (with kg)
-  float* o;            // fp32 [L][Hq][G_tot][d]  attention output of the guide rows
-  float* lse;          // fp32 [L][Hq][G_tot]     natural log of each row's normaliser
-  float2* pstat;       // [nchunk_max + 1][L*Hq*G_tot] per chunk (max, sum), log2 domain; last slot: guide keys
-  float* po;           // [nchunk_max + 1][L*Hq*G_tot][d] per chunk unnormalised output
-  int32_t L, Hq, Hkv, R;
-  int64_t n_tot, g_tot;
-  float c;             // softmax_scale * log2(e)
-  int32_t chunk;       // attn_chunk_tokens of the batch
-  int32_t nchunk_max;  // chunks of the longest sequence
-  int32_t nrg_max;     // row groups of the largest R * G_b
-  BatchArgs bt;
-};
-
-struct AttnWorkspace {
-  size_t pstat_off, po_off, total;
-};
-AttnWorkspace attn_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, int32_t head_dim, const int64_t* ctx_off,
-                                    const int64_t* g_off, int32_t batch);
-hipError_t launch_guide_attention(const AttnArgs& a, int head_dim, hipStream_t stream);
-
 // ---------------------------------------------------------------- step 2 (V scales)
 // The one-multiply multipliers of the format with this qmax, per absmax significand t: the
 // ulp offset from fl32(1/fl32(m/qmax)) (-1, 0, 1), or kNoMultiplier where there is none (also
@@ -148,6 +111,49 @@ hipError_t launch_quantize(const QuantArgs& a, int head_dim, hipStream_t stream)
 // workgroup per CU, one wave per SIMD, at most 48 VGPRs), for running part of step 2 on a
 // second stream concurrently with the score passes.
 hipError_t launch_quantize_lean(const QuantArgs& a, int head_dim, hipStream_t stream);
+
+// ---------------------------------------------------------------- guide rows' prefill attention
+// Context tokens per workgroup of the guide rows' attention: 32768 when every sequence has at
+// least 131072 (fewer partial outputs to merge), else 8192.
+constexpr int kAttnChunkSmall = 8192;
+constexpr int kAttnChunkLarge = 32768;
+inline int32_t attn_chunk_tokens(const int64_t* ctx_off, int32_t batch) {
+  for (int b = 0; b < batch; ++b)
+    if (ctx_off[b + 1] - ctx_off[b] < 131072) return kAttnChunkSmall;
+  return kAttnChunkLarge;
+}
+
+struct AttnArgs {
+  const uint16_t* q;   // bf16 [L][Hq][G_tot][d]
+  const uint16_t* k;   // bf16 [L][Hkv][N_tot][d]
+  const uint16_t* v;   // bf16 [L][Hkv][N_tot][d]
+  const uint16_t* kg;  // bf16 [L][Hkv][G_tot][d] the guide tokens' keys, or nullptr
+  const uint16_t* vg;  // bf16 [L][Hkv][G_tot][d] their values (with kg)
+  float* o;            // fp32 [L][Hq][G_tot][d]  attention output of the guide rows
+  float* lse;          // fp32 [L][Hq][G_tot]     natural log of each row's normaliser
+  float2* pstat;       // [nchunk_max + 1][L*Hq*G_tot] per chunk (max, sum), log2 domain; last slot: guide keys
+  float* po;           // [nchunk_max + 1][L*Hq*G_tot][d] per chunk unnormalised output
+  int32_t L, Hq, Hkv, R;
+  int64_t n_tot, g_tot;
+  float c;             // softmax_scale * log2(e)
+  int32_t chunk;       // attn_chunk_tokens of the batch
+  int32_t nchunk_max;  // chunks of the longest sequence
+  int32_t nrg_max;     // row groups of the largest R * G_b
+  BatchArgs bt;
+  // Step 2 from the staged V sub-tiles (tp_guide_attention_quantize); vq == nullptr: none.
+  float* scales;       // fp32 [L][Hkv][N_tot]
+  uint8_t* vq;         // [L][Hkv][N_tot][row_bytes]
+  int32_t qfmt, bits;
+  float qmax;
+  RecipOffsets ro;     // recip_offsets_for(qmax)
+};
+
+struct AttnWorkspace {
+  size_t pstat_off, po_off, total;
+};
+AttnWorkspace attn_workspace_layout(int32_t L, int32_t Hq, int32_t Hkv, int32_t head_dim, const int64_t* ctx_off,
+                                    const int64_t* g_off, int32_t batch);
+hipError_t launch_guide_attention(const AttnArgs& a, int head_dim, hipStream_t stream);
 
 // ---------------------------------------------------------------- step 3 (select)
 // Every rule but NORM_ADD runs the split selection: each segment's tokens are cut into parts

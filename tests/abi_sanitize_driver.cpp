@@ -330,6 +330,20 @@ void attention_cases() {
   EXPECT(run(a), TP_ERR_WORKSPACE);
   a = base(), a.b = &noguide.c;
   EXPECT(run(a), TP_ERR_NULL);
+  // with step 2 from the same sweep
+  const auto runq = [&](const A& x, int32_t qfmt, int32_t bits, float* sc, void* vq) {
+    return tp_guide_attention_quantize(dp, x.b, x.q, x.k, x.v, x.kg, x.vg, x.scale, qfmt, bits, x.o, x.lse, sc, vq, x.w,
+                                       x.wsb, nullptr);
+  };
+  EXPECT(runq(base(), TP_QFMT_INT, 8, (float*)fake(), nullptr), TP_ERR_NULL);
+  EXPECT(runq(base(), TP_QFMT_INT, 8, nullptr, fake()), TP_ERR_NULL);
+  EXPECT(runq(base(), TP_QFMT_INT, 1, (float*)fake(), fake()), TP_ERR_PARAM);
+  EXPECT(runq(base(), 7, 8, (float*)fake(), fake()), TP_ERR_PARAM);
+  EXPECT(runq(base(), TP_QFMT_INT, 4, (float*)fake(4), fake()), TP_ERR_PARAM);
+  a = base(), a.v = nullptr;
+  EXPECT(runq(a, TP_QFMT_INT, 8, (float*)fake(), fake()), TP_ERR_NULL);
+  a = base(), a.wsb = ws - 1;
+  EXPECT(runq(a, TP_QFMT_FP8_E4M3, 8, (float*)fake(), fake()), TP_ERR_WORKSPACE);
 }
 
 void quantize_select_compact_cases() {
@@ -426,7 +440,11 @@ void evict_cases() {
   EV e = base();
   const auto check = [&](EV ev, tp_status want, int line) { expect(ev.run(), want, "tp_evict", line); };
   e = base(), e.q = nullptr, check(e, TP_ERR_NULL, __LINE__);
-  e = base(), e.v = nullptr, check(e, TP_ERR_NULL, __LINE__);
+  // v = NULL: step 2 done beforehand; its scales and codes must be given
+  e = base(), e.v = nullptr, e.vq = nullptr, check(e, TP_ERR_NULL, __LINE__);
+  e = base(), e.v = nullptr, e.sc = nullptr, check(e, TP_ERR_NULL, __LINE__);
+  e = base(), e.v = nullptr, e.bits = 9, check(e, TP_ERR_PARAM, __LINE__);
+  e = base(), e.v = nullptr, e.vq = fake(4), check(e, TP_ERR_PARAM, __LINE__);
   e = base(), e.vq = nullptr, e.vqout = nullptr, check(e, TP_ERR_NULL, __LINE__);
   e = base(), e.vq = nullptr, e.scout = nullptr, check(e, TP_ERR_NULL, __LINE__);
   e = base(), e.idx = nullptr, check(e, TP_ERR_NULL, __LINE__);
@@ -479,6 +497,10 @@ void well_formed_without_device() {
   EXPECT(tp_guide_attention(&d, &bt.c, fake(), fake(), fake(), fake(), fake(), 0.125f, (float*)fake(), (float*)fake(),
                             fake(), ws_size(TP_FN_GUIDE_ATTENTION, d, bt), nullptr),
          TP_ERR_HIP);
+  EXPECT(tp_guide_attention_quantize(&d, &bt.c, fake(), fake(), fake(), nullptr, nullptr, 0.125f, TP_QFMT_INT, 4,
+                                     (float*)fake(), (float*)fake(), (float*)fake(), fake(), fake(),
+                                     ws_size(TP_FN_GUIDE_ATTENTION, d, bt), nullptr),
+         TP_ERR_HIP);
   EXPECT(tp_quantize_v_scales(&d, &bt.c, fake(), TP_QFMT_INT, 4, (float*)fake(), fake(), nullptr), TP_ERR_HIP);
   EXPECT(tp_combine_select_topk(&d, &bt.c, (const float*)fake(), (const float*)fake(), TP_COMBINE_NORM_ADD, 0.25, 0,
                                 ko.data(), (int32_t*)fake(), nullptr, fake(), ws_size(TP_FN_COMBINE_SELECT_TOPK, d, bt),
@@ -496,7 +518,7 @@ void well_formed_without_device() {
   EXPECT(tp_compact_quantize_kv(&d, &bt.c, ko.data(), (const int32_t*)fake(), fake(), fake(), TP_QFMT_FP8_E4M3, 8, fake(),
                                 fake(), (float*)fake(), nullptr),
          TP_ERR_HIP);
-  for (int mode = 0; mode < 4; ++mode) {
+  for (int mode = 0; mode < 5; ++mode) {
     EV e;
     e.d = &d;
     e.bt = &bt.c;
@@ -505,6 +527,7 @@ void well_formed_without_device() {
     if (mode == 1) e.lse = (const float*)fake();
     if (mode == 2) e.vq = nullptr;
     if (mode == 3) e.rule = TP_COMBINE_NORM_ADD, e.kg = fake();
+    if (mode == 4) e.v = nullptr, e.lse = (const float*)fake();  // step 2 done beforehand
     EXPECT(e.run(), TP_ERR_HIP);
   }
 }

@@ -234,6 +234,33 @@ def test_guide_attention_validation():
 
 
 @no_gpu
+def test_guide_attention_quantize_validation():
+    d = B.dims(2, 8, 2, 64)
+    bt = B.Batch([0, 100, 300], [0, 16, 20])
+    ws = B.tp_workspace_size(B.TP_FN_GUIDE_ATTENTION, d, bt)
+
+    def attq(q=FAKE, k=FAKE, v=FAKE, kg=None, vg=None, scale=0.125, fmt=0, bits=8, o_=FAKE, lse=FAKE, sc=FAKE,
+             vq=FAKE, w=FAKE, wsb=ws, batch=bt):
+        return lib.tp_guide_attention_quantize(ctypes.byref(d), ctypes.byref(batch.c), q, k, v, kg, vg, scale, fmt,
+                                               bits, o_, lse, sc, vq, w, wsb, None)
+
+    assert attq(v=None) == B.TP_ERR_NULL
+    assert attq(sc=None) == B.TP_ERR_NULL
+    assert attq(vq=None) == B.TP_ERR_NULL       # the codes are always written
+    assert attq(lse=None) == B.TP_ERR_NULL
+    assert attq(kg=FAKE) == B.TP_ERR_NULL
+    assert attq(fmt=3) == B.TP_ERR_PARAM
+    assert attq(bits=1) == B.TP_ERR_PARAM
+    assert attq(bits=9) == B.TP_ERR_PARAM
+    assert attq(sc=FAKE + 4) == B.TP_ERR_PARAM
+    assert attq(vq=FAKE + 8) == B.TP_ERR_PARAM
+    assert attq(scale=-1.0) == B.TP_ERR_PARAM
+    assert attq(wsb=ws - 1) == B.TP_ERR_WORKSPACE
+    assert attq(batch=B.Batch([0, 100, 300])) == B.TP_ERR_NULL
+    assert lib.tp_last_error().decode() != ""
+
+
+@no_gpu
 def test_compact_validation():
     d = B.dims(2, 8, 2, 64)
     bt = B.Batch([0, 100, 300])
@@ -272,7 +299,13 @@ def test_evict_validation():
     null_prof = B.TpProfile(B.TP_EVICT_EVENTS)
     cases = [
         (dict(q=None), B.TP_ERR_NULL),
-        (dict(v=None), B.TP_ERR_NULL),
+        # v = NULL: step 2 done beforehand, scales and codes are inputs and must be given
+        (dict(v=None, vq=None), B.TP_ERR_NULL),
+        (dict(v=None, vq=None, vqout=None), B.TP_ERR_NULL),
+        (dict(v=None, sc=None), B.TP_ERR_NULL),
+        (dict(v=None, vq=FAKE + 4), B.TP_ERR_PARAM),
+        (dict(v=None, bits=9), B.TP_ERR_PARAM),
+        (dict(v=None, qfmt=5), B.TP_ERR_PARAM),
         (dict(vq=None, vqout=None), B.TP_ERR_NULL),  # without v_q the kept rows are quantised: v_q_out needed
         (dict(vq=None, scout=None), B.TP_ERR_NULL),
         (dict(idx=None), B.TP_ERR_NULL),
