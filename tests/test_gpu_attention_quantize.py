@@ -166,3 +166,28 @@ def test_attention_quantize_fullsize(gpu_lib):
             assert np.array_equal(scales[r0:r1].cpu().numpy().view(np.uint32), g_ref), (l, h, t0)
             assert np.array_equal(vq[r0 * rb:r1 * rb].cpu().numpy().reshape(t1 - t0, rb), c_ref), (l, h, t0)
     pu.log("  full-size scales and codes equal to tp_quantize_v_scales; sampled rows match the oracle")
+
+
+@pytest.mark.parametrize("rule", [B.TP_COMBINE_NORM_ADD, B.TP_COMBINE_HARMONIC], ids=["norm-add", "harmonic"])
+def test_evict_without_v_rules_and_pass1(gpu_lib, rule):
+    """tp_evict(v = NULL) with step 2 from tp_quantize_v_scales and both score passes (no
+    normalisers given), under the rules whose pooling runs in its own kernel (normalised add)
+    or in the selection (harmonic): bit-identical to tp_evict(v), with the profile events."""
+    w = _workload(CASES[0])
+    pu.log(f"evict without V, both passes, rule {rule}: {w.describe()}")
+    q, k, v = pu.device_inputs(w)
+    d = B.dims(w.L, w.Hq, w.Hkv, w.d)
+    bt = B.Batch(w.ctx_offsets(), w.guide_offsets())
+    kw = dict(softmax_scale=w.softmax_scale, pool_k=w.pool_k, qfmt=w.qfmt, bits=w.bits, rule=rule,
+              keep_ratio=w.keep_ratio or 0.0, keep_budget=w.keep_budget or 0)
+    ref = B.evict_fused(d, bt, q, k, v, **kw)
+    bufs = B.EvictBuffers(d, bt, w.qfmt, w.bits, ref.kept_offsets, device=k.device)
+    B.tp_quantize_v_scales(d, bt, v, w.qfmt, w.bits, bufs.scales, bufs.v_q)
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(B.TP_EVICT_EVENTS)]
+    B.evict_fused(d, bt, q, k, None, **kw, bufs=bufs, events=events)
+    torch.cuda.synchronize()
+    for name in ("s_key", "scales", "v_q", "s_comb", "kept_idx", "k_c", "v_q_c", "scales_c"):
+        a, b = getattr(bufs, name), getattr(ref, name)
+        assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), name + " differs"
+    ms = [events[i].elapsed_time(events[i + 1]) for i in range(B.TP_EVICT_EVENTS - 1)]
+    assert all(t >= 0.0 for t in ms), ms
