@@ -270,8 +270,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
   constexpr int RING = AC::kRing;
   constexpr bool QUANT = QK != kAttnNoQuant;
   constexpr int QKC = QUANT ? QK : 0;
-  constexpr int LPT = D / 8;     // lanes per V row in the quantisation
-  constexpr int RPW = 64 / LPT;  // rows per wave
+  constexpr int QNP = D / 64;     // the quantisation: 16-byte pieces of a V row per lane,
+  constexpr int QLPT = 8;         // lanes per row (8 rows per wave)
   // the ring, then (QUANT) the quantisation tables
   __shared__ __attribute__((aligned(1024))) char ring[RING * AC::kSlotBytes + (QUANT ? sizeof(QuantTables) : 0)];
   QuantTables& tab = *(QuantTables*)(ring + RING * AC::kSlotBytes);
@@ -414,26 +414,32 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) pb[s2][jj] = (__bf16)p[8 * s2 + jj];
   };
-  // Step 2 of the token rows of sub-tile x (ring slot sl), RPW rows per wave: read from the
-  // staged V tile, quantised, scale and codes stored.  Only the workgroup of the chunk's
-  // first row group does this, in waves 0 .. 32 / RPW - 1.  Its stores are vector-memory
-  // operations like the ring's copies and may complete out of order with them, so a wave
-  // that quantises waits for all of its memory operations at each barrier (vmcnt(0)), which
-  // leaves each pair's copies the pair's duration to land.
-  const bool qwave = QUANT && !u.guide && u.rg == 0 && wave < 32 / RPW;
+  // Step 2 of the token rows of a pair of sub-tiles: waves 0-3 take sub-tile t, 4-7 sub-tile
+  // t + 1, 8 rows each, a lane QNP adjacent 16-byte pieces of its row; read from the staged V
+  // tile, quantised, scale and codes stored.  Only the workgroup of the chunk's first row
+  // group does this.  Its stores are vector-memory operations like the ring's copies and may
+  // complete out of order with them, so this instance waits for all of a wave's memory
+  // operations at each barrier (vmcnt(0)), which leaves each pair's copies the pair's
+  // duration to land.
+  const bool qwg = QUANT && !u.guide && u.rg == 0;
   const QuantFmt qfmt{a.qfmt == TP_QFMT_INT, a.qfmt == TP_QFMT_INT && a.bits <= 4, a.qmax};
   const int64_t qrow0 = (int64_t)u.seg * a.n_tot + u.n0 + (int64_t)u.chunk * a.chunk;
-  const auto quant_sub = [&](int x, int sl) {
-    const int tl = wave * RPW + lane / LPT;
-    const int p = lane % LPT;
-    const char* vt = ring + sl * AC::kSlotBytes + AC::kTileBytes;
-    const uint4 xv = *(const uint4*)(vt + tl * C::kRowBytes + ((p ^ swzv<D>(tl)) << 4));
-    uint2 cd;
-    const float gamma = quant_piece<LPT, QKC>(xv, tab, qfmt, cd);
-    const int tok = 32 * x + tl;
+  const int qtl = 8 * (wave & 3) + lane / QLPT;  // the lane's row of its sub-tile
+  const int qj = lane % QLPT;                     // and its first piece, QNP qj
+  const auto quant_pair = [&](int t, int cur, int c1) {
+    const int x = t + (wave >> 2);
+    if (x >= nsub) return;  // wave-uniform
+    const char* vt = ring + (wave < 4 ? cur : c1) * AC::kSlotBytes + AC::kTileBytes + qtl * C::kRowBytes;
+    uint4 xv[QNP];
+#pragma unroll
+    for (int n = 0; n < QNP; ++n) xv[n] = *(const uint4*)(vt + (((QNP * qj + n) ^ swzv<D>(qtl)) << 4));
+    uint2 cd[QNP];
+    const float gamma = quant_pieces<QLPT, QKC, QNP>(xv, tab, qfmt, cd);
+    const int tok = 32 * x + qtl;
     if (tok < ntok) {  // rows past the chunk's end repeat its last row
-      if (p == 0) a.scales[qrow0 + tok] = gamma;
-      store_codes<D, QKC>(a.vq, qrow0 + tok, p, cd);
+      const int64_t row = qrow0 + tok;
+      if (qj == 0) a.scales[row] = gamma;
+      store_code_pieces<D, QKC, QNP>(a.vq, row, qj, cd);
     }
   };
   using Full = std::integral_constant<bool, true>;
@@ -450,10 +456,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
       const int f2 = cur >= 1 ? cur - 1 : cur + RING - 1;
       copy_whole<D>(kb, vb, 32 * (t + RING - 1), cvoff, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
       const int c1 = cur + 1 == RING ? 0 : cur + 1;
-      if (qwave) {
-        quant_sub(t, cur);
-        quant_sub(t + 1, c1);
-      }
+      if (qwg) quant_pair(t, cur, c1);
       if (active) {
         iteration(t, cur, sc, sc2, Full{});
         iteration(t + 1, c1, sc2, sc, Full{});
@@ -476,10 +479,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void k_guide_fwd(AttnArgs a) {
     if (t + RING - 1 < nsub)
       copy_subtile<D>(kb, vb, 32 * (t + RING - 1), ntok, ring_lds + (uint32_t)(f2 * AC::kSlotBytes), wave);
     const int c1 = cur + 1 == RING ? 0 : cur + 1;
-    if (qwave) {
-      quant_sub(t, cur);
-      if (t + 1 < nsub) quant_sub(t + 1, c1);
-    }
+    if (qwg) quant_pair(t, cur, c1);
     if (active) {
       iteration(t, cur, sc, sc2, Any{});
       if (t + 1 < nsub) iteration(t + 1, c1, sc2, sc, Any{});

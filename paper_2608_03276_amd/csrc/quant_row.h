@@ -318,6 +318,101 @@ __device__ inline float quant_piece(const uint4& x, const QuantTables& tab, cons
   return gamma;
 }
 
+// quant_piece for NP consecutive 16-byte pieces per lane (8 NP bf16 values; a row's D/8
+// pieces in LPT = D/(8 NP) consecutive lanes): the same arithmetic and the same per-wave path
+// choice, with the row's per-lane work (absmax reduction, table lookup, path tests) shared by
+// the NP pieces.  Returns gamma and each piece's codes in out[n], as quant_piece.  The
+// quantisation kernels keep quant_piece's own one-piece form: the lean kernel's register
+// count, on which its fit beside the score passes depends, is that form's.
+template <int LPT, int K, int NP>
+__device__ inline float quant_pieces(const uint4 (&x)[NP], const QuantTables& tab, const QuantFmt& f,
+                                     uint2 (&out)[NP]) {
+  uint32_t w[NP][4];
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 m2 = {0, 0};  // the lane's largest magnitude, two per packed max
+#pragma unroll
+  for (int n = 0; n < NP; ++n) {
+    w[n][0] = x[n].x;
+    w[n][1] = x[n].y;
+    w[n][2] = x[n].z;
+    w[n][3] = x[n].w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, w[n][i] & 0x7FFF7FFFu));
+  }
+  const uint32_t mx = group_max<LPT>(max((uint32_t)m2.x, (uint32_t)m2.y));
+  const int ef = (int)(mx >> 7);
+  uint32_t code[NP][8];
+  float gamma;
+  if (__builtin_amdgcn_ballot_w64(ef < kFastExpLo || ef > kFastExpHi) == 0) {
+    const int t = (int)(mx & 0x7Fu);
+    gamma = __builtin_amdgcn_ldexpf(tab.g[t], ef - 127);
+    const float ym = tab.ym[t];
+    if (K == kQInt8) {  // every int8 significand has a multiplier
+      const float ys = __builtin_amdgcn_ldexpf(ym, 127 - ef);
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_fast_int8(w[n], ys, code[n]);
+    } else if (__builtin_amdgcn_ballot_w64(!(ym > 0.0f)) == 0) {
+      const float ys = __builtin_amdgcn_ldexpf(ym, 127 - ef);
+      if (K == kQE4M3) {
+#pragma unroll
+        for (int n = 0; n < NP; ++n) out[n] = codes_mul_e4m3(w[n], ys);
+        return gamma;
+      }
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_mul(w[n], ys, code[n]);
+    } else {
+      const float ys = __builtin_amdgcn_ldexpf(tab.y[t], 127 - ef);
+      if (K == kQE4M3) {
+#pragma unroll
+        for (int n = 0; n < NP; ++n) out[n] = codes_fast_e4m3(w[n], gamma, ys);
+        return gamma;
+      }
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_fast<K>(w[n], gamma, ys, code[n]);
+    }
+  } else {
+    const float amax = __uint_as_float(mx << 16);
+    gamma = amax / f.qmax;
+    // below 2^-100 (zero rows included) the division path is taken, for the whole wave
+    // when any lane needs it
+    if (__builtin_amdgcn_ballot_w64(ef <= 27) == 0) {
+      const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+      const float gs = gamma * sc;
+      const float ys = 1.0f / gs;
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_scaled(w[n], sc, gs, ys, f, code[n]);
+    } else if (ef <= 27) {
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_divided(w[n], gamma, f, code[n]);
+    } else {
+      const float sc = __builtin_amdgcn_ldexpf(1.0f, 127 - ef);
+      const float gs = gamma * sc;
+      const float ys = 1.0f / gs;
+#pragma unroll
+      for (int n = 0; n < NP; ++n) codes_scaled(w[n], sc, gs, ys, f, code[n]);
+    }
+  }
+#pragma unroll
+  for (int n = 0; n < NP; ++n) {
+    if (K == kQNibble) {
+      uint32_t p = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) p |= (code[n][i] & 0xFu) << (4 * i);
+      out[n].x = p;
+      out[n].y = 0;
+    } else {
+      // bytes 0 of (c0, c1, c2, c3) -> one dword, via two byte permutes and a word merge
+      const uint32_t lo01 = __builtin_amdgcn_perm(code[n][1], code[n][0], 0x0c0c0400u);
+      const uint32_t lo23 = __builtin_amdgcn_perm(code[n][3], code[n][2], 0x0c0c0400u);
+      const uint32_t hi01 = __builtin_amdgcn_perm(code[n][5], code[n][4], 0x0c0c0400u);
+      const uint32_t hi23 = __builtin_amdgcn_perm(code[n][7], code[n][6], 0x0c0c0400u);
+      out[n].x = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
+      out[n].y = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
+    }
+  }
+  return gamma;
+}
+
 // Store the codes of one piece: row `row` of a code tensor with `row_bytes` per row, piece
 // `sub` (D/8 pieces per row).  Nontemporal: the codes are streamed out, not re-read here.
 template <int D, int K>
@@ -330,6 +425,29 @@ __device__ inline void store_codes(uint8_t* vq, int64_t row, int sub, const uint
     t.x = c.x;
     t.y = c.y;
     __builtin_nontemporal_store(t, (u32x2*)(vq + row * D) + sub);
+  }
+}
+
+// Store the codes of NP adjacent pieces, the lane's j-th group of NP in row `row`, at once.
+template <int D, int K, int NP>
+__device__ inline void store_code_pieces(uint8_t* vq, int64_t row, int j, const uint2 (&c)[NP]) {
+  typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  static_assert(NP == 1 || NP == 2, "one or two pieces");
+  if (NP == 1) {
+    store_codes<D, K>(vq, row, j, c[0]);
+  } else if (K == kQNibble) {
+    u32x2 t;
+    t.x = c[0].x;
+    t.y = c[NP - 1].x;
+    __builtin_nontemporal_store(t, (u32x2*)(vq + row * (D / 2)) + j);
+  } else {
+    u32x4 t;
+    t.x = c[0].x;
+    t.y = c[0].y;
+    t.z = c[NP - 1].x;
+    t.w = c[NP - 1].y;
+    __builtin_nontemporal_store(t, (u32x4*)(vq + row * D) + j);
   }
 }
 
