@@ -22,6 +22,9 @@
 //       operand comes from the token-major V sub-tile through transposing LDS reads.
 // Each workgroup writes its rows' partial (max, sum) and unnormalised O; the guide's own keys
 // are one more chunk, with the causal mask.  A merge kernel combines the chunks.
+// An instance per code format also performs step 2 (Eq. 2, Sec. 3.3) on the V sub-tiles it
+// stages (tp_guide_attention_quantize), so the quantised cache and the value scores come from
+// this one read of V.
 #include "quant_row.h"
 #include "tile_common.h"
 #include "tp_internal.h"
