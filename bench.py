@@ -89,6 +89,19 @@ def algorithmic_bytes(w, kept_total_per_head, full_codes=True, normalisers_given
     return per, path
 
 
+def attention_bytes(w, with_step2: bool) -> int:
+    """Compulsory HBM bytes of the guide rows' attention (k_guide_fwd and its merge): K and V
+    of the context and the guide tokens and Q read, O written (the normalisers are a rounding
+    error), plus, with step 2 inside it, every context token's V codes and scale written."""
+    from paper_2608_03276_amd import binding as B
+
+    LH = w.L * w.Hkv
+    b = (2 * LH * w.n_tot * w.d * 2 + w.L * w.Hq * w.g_tot * w.d * (2 + 4) + 2 * LH * w.g_tot * w.d * 2)
+    if with_step2:
+        b += LH * w.n_tot * (B.row_bytes(w.qfmt, w.bits, w.d) + 4)
+    return b
+
+
 # k_quantize_lean launches per tp_evict call, without / with the normalisers given, and the
 # rows of each launch as a fraction of all rows, by (normalisers given, full codes)
 LEAN_LAUNCHES = {False: 2, True: 1}
@@ -459,10 +472,7 @@ def main():
     # a score pass), over K and V once each
     attn_flops = 2 * score_flops + (4 * w.L * w.Hq * sum(g * (g + 1) // 2 for g in w.guide_lens) * w.d
                                     if args.prefill_attention else 0)
-    per["k_guide_fwd"] = (2 * w.L * w.Hkv * w.n_tot * w.d * 2 + w.L * w.Hq * w.g_tot * w.d * (2 + 4)
-                          + 2 * w.L * w.Hkv * w.g_tot * w.d * 2)  # K, V, Q and guide K/V read; O written
-    if args.prefill_attention:  # with step 2: V's codes and scales written
-        per["k_guide_fwd"] += w.L * w.Hkv * w.n_tot * (B.row_bytes(w.qfmt, w.bits, w.d) + 4)
+    per["k_guide_fwd"] = attention_bytes(w, args.prefill_attention)
 
     def roofline_of(kern):
         # the roof is whichever of HBM bytes and matrix flops takes longer at its peak; the

@@ -67,3 +67,16 @@ def test_kernel_source_lists_name_existing_files():
     for kernel, names in bench.KERNEL_SOURCES.items():
         for name in names:
             assert os.path.exists(os.path.join(ROOT, "paper_2608_03276_amd", "csrc", name)), (kernel, name)
+
+
+def test_attention_bytes_128k():
+    """The guide rows' attention at 128K, counted by hand: K and V of the context
+    (2 x 32 x 8 x 131072 x 128 x 2 B), Q (32 x 32 x 64 x 128 x 2 B) and O (x 4 B), the
+    guide tokens' K and V (2 x 32 x 8 x 64 x 128 x 2 B); with step 2, int8 codes and a
+    4-byte scale per context token-head."""
+    w = W.llama8b_128k()
+    plain = 17_179_869_184 + 16_777_216 + 33_554_432 + 8_388_608
+    assert bench.attention_bytes(w, False) == plain
+    assert bench.attention_bytes(w, True) == plain + 32 * 8 * 131072 * (128 + 4) == 21_667_774_464
+    w4 = w.with_(bits=4)  # nibbles: 64 code bytes per row
+    assert bench.attention_bytes(w4, True) == plain + 32 * 8 * 131072 * (64 + 4)
