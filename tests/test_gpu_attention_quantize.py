@@ -191,3 +191,23 @@ def test_evict_without_v_rules_and_pass1(gpu_lib, rule):
         assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), name + " differs"
     ms = [events[i].elapsed_time(events[i + 1]) for i in range(B.TP_EVICT_EVENTS - 1)]
     assert all(t >= 0.0 for t in ms), ms
+
+
+@pytest.mark.parametrize("bits", [2, 3, 5, 7])
+def test_attention_quantize_bit_widths(gpu_lib, bits):
+    """The integer widths the cases above leave out (each has its own qmax and its own
+    one-multiply multipliers or fallbacks): scales and codes bit-exact against the oracle,
+    with the planted rows, on a batch with a ragged tail and two row groups."""
+    case = (f"int{bits}", 1, 16, 2, 128, [3001, 64], [40, 3], False, INT, bits)
+    w = _workload(case)
+    pu.log(f"attention + quantisation, int{bits}: {w.describe()}")
+    q, k, v = pu.device_inputs(w)
+    _plant(v, w.d)
+    (o_ref, l_ref), (o_q, l_q), scales, vq = _run(w, q, k, v, None, None)
+    assert torch.equal(o_q.view(torch.int32), o_ref.view(torch.int32)), "attention output differs"
+    g_ref, c_ref = _oracle_quant(v.view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1, w.d), w.qfmt, w.bits)
+    g_gpu = scales.cpu().numpy().view(np.uint32)
+    c_gpu = vq.cpu().numpy().reshape(g_gpu.shape[0], -1)
+    assert np.array_equal(g_gpu, g_ref), f"{int(np.sum(g_gpu != g_ref))} scales differ"
+    bad = np.nonzero(np.any(c_gpu != c_ref, axis=1))[0]
+    assert bad.size == 0, f"{bad.size} code rows differ, first rows {bad[:8].tolist()}"
